@@ -1,0 +1,342 @@
+/*
+ * mori_oracle.c -- plain CPU oracle for MORI's idleness-ranked KV tier placement
+ * (arXiv 2606.00866).  TEST INFRASTRUCTURE ONLY: used by the tests, the smoke
+ * check and the benchmark's CPU-baseline leg, never by the product path.
+ *
+ * Deliberately simple: whole-array loops in the order the paper describes the
+ * method, a library sort, memcpy per KV run.  No blocking, fusion or
+ * reordering beyond what the definitions state.  Readings of points the paper
+ * leaves open are marked "Reading:".
+ */
+#include "mori_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------ */
+/* Step 1 -- idleness, Eq. 1 (Sec. 4.2 "Idleness Metric").                   */
+/*   iota = T_acting / (T_reasoning + T_acting), both totals over the last k   */
+/*   reasoning/tool-call cycles, the ongoing call's elapsed time included.     */
+/* Reading: binary32 throughout; each total is accumulated oldest cycle first */
+/* starting from +0; a program with no recorded time (denominator 0) gets     */
+/* idleness 0; a zero result is +0.  Inputs must be finite and >= 0 and the    */
+/* totals must stay finite, otherwise the program data is rejected.          */
+/* ------------------------------------------------------------------------ */
+int orc_idleness(uint32_t P, uint32_t k, const float* window, float* iota) {
+  for (uint32_t p = 0; p < P; ++p) {
+    float t_reasoning = 0.0f;
+    float t_acting = 0.0f;
+    for (uint32_t j = 0; j < k; ++j) {
+      float r = window[((size_t)p * k + j) * 2 + 0];
+      float a = window[((size_t)p * k + j) * 2 + 1];
+      if (!(r >= 0.0f) || !(a >= 0.0f) || isinf(r) || isinf(a)) return ORC_E_INPUT;
+      t_reasoning = t_reasoning + r;
+      t_acting = t_acting + a;
+    }
+    float total = t_reasoning + t_acting;
+    if (isinf(t_reasoning) || isinf(t_acting) || isinf(total)) return ORC_E_INPUT;
+    float value = (total > 0.0f) ? t_acting / total : 0.0f;
+    if (value == 0.0f) value = 0.0f; /* drop the sign of a negative zero */
+    iota[p] = value;
+  }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Ranking key.  Programs are ranked busiest (lowest idleness) first.        */
+/* Reading: the key is the binary32 bit pattern of idleness, which orders    */
+/* like the value because idleness lies in [0, 1].  With ORC_F_STATUS_KEY an */
+/* Acting program (status 1) is placed after every Reasoning program, since  */
+/* Acting programs are demoted first (Sec. 4.3.1, demotion from GPU).        */
+/* ------------------------------------------------------------------------ */
+int orc_keys(uint32_t P, const float* iota, const uint8_t* status, uint32_t flags, uint32_t* key) {
+  for (uint32_t p = 0; p < P; ++p) {
+    float v = iota[p];
+    if (!(v >= 0.0f && v <= 1.0f)) return ORC_E_INPUT;
+    if (v == 0.0f) v = 0.0f;
+    uint32_t bits;
+    memcpy(&bits, &v, sizeof bits);
+    if ((flags & ORC_F_STATUS_KEY) && status != NULL && status[p] == 1) bits |= 0x80000000u;
+    key[p] = bits;
+  }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Relative ranking (Sec. 1, Sec. 4.3): order all programs by key.          */
+/* Reading: ties go to the lower program id, i.e. the sort is on the pair    */
+/* (key, id), which is a total order.                                        */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+  uint32_t key, id;
+} orc_pair;
+
+static int orc_pair_cmp(const void* a, const void* b) {
+  const orc_pair* x = (const orc_pair*)a;
+  const orc_pair* y = (const orc_pair*)b;
+  if (x->key != y->key) return x->key < y->key ? -1 : 1;
+  if (x->id != y->id) return x->id < y->id ? -1 : 1;
+  return 0;
+}
+
+void orc_order(uint32_t P, const uint32_t* key, uint32_t* order, uint32_t* rank) {
+  orc_pair* pairs = (orc_pair*)malloc(sizeof(orc_pair) * (P ? P : 1));
+  for (uint32_t p = 0; p < P; ++p) {
+    pairs[p].key = key[p];
+    pairs[p].id = p;
+  }
+  qsort(pairs, P, sizeof(orc_pair), orc_pair_cmp);
+  for (uint32_t r = 0; r < P; ++r) {
+    order[r] = pairs[r].id;
+    if (rank) rank[pairs[r].id] = r;
+  }
+  free(pairs);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Capacity-matched boundary (Sec. 1; Sec. 4.1 three-tier queues and their   */
+/* capacity invariants; Sec. 7.2: fill from the busiest end of the ranking   */
+/* until capacity is reached).                                               */
+/* Reading: a program is placed whole (never split across tiers) with       */
+/* ceil(context/tokens-per-block) blocks; the boundary is a strict prefix of */
+/* the ranking: the GPU tier takes the longest prefix whose bytes do not     */
+/* exceed the GPU budget, the CPU tier the longest following run that does   */
+/* not exceed the CPU budget, the rest go to Waiting.  ORC_F_SKIP_FIT walks  */
+/* the ranking once and puts each program in the first tier it still fits.  */
+/* ------------------------------------------------------------------------ */
+void orc_boundary(uint32_t P, const uint32_t* order, const uint32_t* nblk, uint64_t block_bytes,
+                  uint64_t gpu_budget, uint64_t cpu_budget, uint32_t flags, uint64_t* prefix,
+                  uint8_t* tier_new, uint32_t* m_gpu, uint32_t* m_cpu) {
+  uint64_t running = 0;
+  for (uint32_t r = 0; r < P; ++r) {
+    running += (uint64_t)nblk[order[r]] * block_bytes;
+    prefix[r] = running;
+  }
+  uint32_t n_gpu = 0, n_cpu = 0;
+  if (flags & ORC_F_SKIP_FIT) {
+    uint64_t room_gpu = gpu_budget, room_cpu = cpu_budget;
+    for (uint32_t r = 0; r < P; ++r) {
+      uint32_t p = order[r];
+      uint64_t bytes = (uint64_t)nblk[p] * block_bytes;
+      if (bytes <= room_gpu) {
+        room_gpu -= bytes;
+        tier_new[p] = ORC_GPU;
+        ++n_gpu;
+      } else if (bytes <= room_cpu) {
+        room_cpu -= bytes;
+        tier_new[p] = ORC_CPU;
+        ++n_cpu;
+      } else {
+        tier_new[p] = ORC_WAIT;
+      }
+    }
+  } else {
+    while (n_gpu < P && prefix[n_gpu] <= gpu_budget) ++n_gpu;
+    uint64_t gpu_part = n_gpu ? prefix[n_gpu - 1] : 0;
+    while (n_gpu + n_cpu < P && prefix[n_gpu + n_cpu] - gpu_part <= cpu_budget) ++n_cpu;
+    for (uint32_t r = 0; r < P; ++r) {
+      uint32_t p = order[r];
+      tier_new[p] = (r < n_gpu) ? ORC_GPU : (r < n_gpu + n_cpu) ? ORC_CPU : ORC_WAIT;
+    }
+  }
+  *m_gpu = n_gpu;
+  *m_cpu = n_cpu;
+}
+
+static uint8_t orc_category(uint8_t from, uint8_t to) {
+  if (from == to) return ORC_KEPT;
+  if (from == ORC_GPU) return to == ORC_CPU ? ORC_OUT : ORC_DROP_GPU;
+  if (from == ORC_CPU) return to == ORC_GPU ? ORC_IN : ORC_DROP_CPU;
+  return to == ORC_GPU ? ORC_ADMIT_GPU : ORC_ADMIT_CPU;
+}
+
+/* ------------------------------------------------------------------------ */
+/* One rebalance.                                                            */
+/* ------------------------------------------------------------------------ */
+int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32_t k,
+                  const float* window, const float* iota_given, const uint8_t* status,
+                  const uint32_t* tbl_off, uint32_t tbl_len, uint32_t* tbl, uint8_t* tier,
+                  uint8_t* free_map, uint64_t gpu_budget, uint64_t cpu_budget, uint32_t flags,
+                  uint8_t* const* host_bufs, uint32_t* order_out, uint32_t* rank_out,
+                  uint8_t* tier_old_out, uint8_t* category_out, uint64_t* prefix_out,
+                  orc_summary* summary) {
+  const uint32_t NB = g->num_blocks;
+  const uint64_t planes = (uint64_t)g->layers * g->planes;
+  const uint64_t run = (uint64_t)g->block_tokens * g->row_bytes; /* bytes of one (plane, page) */
+  const uint64_t block_bytes = planes * run;                      /* bytes of one page, all planes */
+  const size_t np = P ? P : 1;
+  int rc = ORC_OK;
+
+  float* iota = (float*)calloc(np, sizeof(float));
+  uint32_t* key = (uint32_t*)malloc(sizeof(uint32_t) * np);
+  uint32_t* order = (uint32_t*)malloc(sizeof(uint32_t) * np);
+  uint32_t* rank = (uint32_t*)malloc(sizeof(uint32_t) * np);
+  uint32_t* nblk = (uint32_t*)malloc(sizeof(uint32_t) * np);
+  uint64_t* prefix = (uint64_t*)malloc(sizeof(uint64_t) * np);
+  uint8_t* tier_new = (uint8_t*)malloc(np);
+  uint8_t* cat = (uint8_t*)malloc(np);
+  uint8_t* page_state = (uint8_t*)calloc(NB ? NB : 1, 1); /* bit0 free, bit1 owned, bit2 released */
+  uint32_t* pages_avail = (uint32_t*)malloc(sizeof(uint32_t) * (NB ? NB : 1));
+  uint32_t* new_tbl = NULL;
+
+  /* -- program data: tiers and the block-table offsets -- */
+  for (uint32_t p = 0; p < P && rc == ORC_OK; ++p)
+    if (tier[p] > ORC_WAIT) rc = ORC_E_INPUT;
+  if (rc == ORC_OK && tbl_off[0] != 0) rc = ORC_E_INPUT;
+  for (uint32_t p = 0; p < P && rc == ORC_OK; ++p) {
+    if (tbl_off[p + 1] < tbl_off[p]) rc = ORC_E_INPUT;
+    else nblk[p] = tbl_off[p + 1] - tbl_off[p];
+  }
+  if (rc == ORC_OK && tbl_off[P] > tbl_len) rc = ORC_E_INPUT;
+
+  /* -- steps 1-3: idleness, ranking, boundary -- */
+  if (rc == ORC_OK) {
+    if (flags & ORC_F_IDLENESS_GIVEN) {
+      for (uint32_t p = 0; p < P; ++p) iota[p] = iota_given[p];
+    } else {
+      rc = orc_idleness(P, k, window, iota);
+    }
+  }
+  if (rc == ORC_OK) rc = orc_keys(P, iota, status, flags, key);
+  uint32_t m_gpu = 0, m_cpu = 0;
+  if (rc == ORC_OK) {
+    orc_order(P, key, order, rank);
+    orc_boundary(P, order, nblk, block_bytes, gpu_budget, cpu_budget, flags, prefix, tier_new,
+                 &m_gpu, &m_cpu);
+    for (uint32_t p = 0; p < P; ++p) cat[p] = orc_category(tier[p], tier_new[p]);
+  }
+
+  /* -- pool consistency: every page is either free or owned by exactly one
+        GPU-resident program; non-resident programs hold no page -- */
+  if (rc == ORC_OK) {
+    for (uint32_t pg = 0; pg < NB; ++pg)
+      if (free_map[pg]) page_state[pg] |= 1u;
+    for (uint32_t p = 0; p < P && rc == ORC_OK; ++p) {
+      for (uint32_t i = 0; i < nblk[p] && rc == ORC_OK; ++i) {
+        uint32_t pg = tbl[tbl_off[p] + i];
+        if (tier[p] != ORC_GPU) {
+          if (pg != ORC_NONE) rc = ORC_E_POOL;
+          continue;
+        }
+        if (pg >= NB || (page_state[pg] & 3u)) {
+          rc = ORC_E_POOL;
+          continue;
+        }
+        page_state[pg] |= 2u;
+        if (cat[p] == ORC_OUT || cat[p] == ORC_DROP_GPU) page_state[pg] |= 4u;
+      }
+    }
+    for (uint32_t pg = 0; pg < NB && rc == ORC_OK; ++pg)
+      if (!(page_state[pg] & 3u)) rc = ORC_E_POOL;
+  }
+  if (rc == ORC_OK && pool_bytes && host_bufs) {
+    for (uint32_t p = 0; p < P && rc == ORC_OK; ++p)
+      if ((cat[p] == ORC_OUT || cat[p] == ORC_IN) && nblk[p] && host_bufs[p] == NULL) rc = ORC_E_INPUT;
+  }
+
+  /* -- step 4: page allocation (Reading: pages free before this step in
+        ascending id order, then the pages released by programs leaving the
+        GPU in ascending id order; they are handed out first to the programs
+        promoted from the CPU tier, then to those admitted from Waiting,
+        following the promotion priority of Sec. 4.3.1, each group in rank
+        order, each program's blocks in logical order) -- */
+  uint64_t n_free0 = 0, n_rel = 0, need = 0;
+  if (rc == ORC_OK) {
+    for (uint32_t pg = 0; pg < NB; ++pg)
+      if (page_state[pg] & 1u) pages_avail[n_free0++] = pg;
+    for (uint32_t pg = 0; pg < NB; ++pg)
+      if (page_state[pg] & 4u) pages_avail[n_free0 + n_rel++] = pg;
+    for (uint32_t p = 0; p < P; ++p)
+      if (cat[p] == ORC_IN || cat[p] == ORC_ADMIT_GPU) need += nblk[p];
+    if (need > n_free0 + n_rel) rc = ORC_E_NOSPC;
+  }
+
+  if (rc == ORC_OK) {
+    /* -- step 5a: swap-out, reading the tables as they were before this step -- */
+    if (pool_bytes && host_bufs) {
+      for (uint32_t p = 0; p < P; ++p) {
+        if (cat[p] != ORC_OUT) continue;
+        for (uint64_t q = 0; q < planes; ++q)
+          for (uint32_t i = 0; i < nblk[p]; ++i) {
+            uint64_t page = tbl[tbl_off[p] + i];
+            memcpy(host_bufs[p] + (q * nblk[p] + i) * run, pool_bytes + (q * NB + page) * run, run);
+          }
+      }
+    }
+    /* -- table rewrite and the free map after the step -- */
+    new_tbl = (uint32_t*)malloc(sizeof(uint32_t) * (tbl_off[P] ? tbl_off[P] : 1));
+    memcpy(new_tbl, tbl, sizeof(uint32_t) * tbl_off[P]);
+    uint64_t slot = 0;
+    for (int pass = 0; pass < 2; ++pass) {
+      uint8_t want = pass == 0 ? ORC_IN : ORC_ADMIT_GPU;
+      for (uint32_t r = 0; r < P; ++r) {
+        uint32_t p = order[r];
+        if (cat[p] != want) continue;
+        for (uint32_t i = 0; i < nblk[p]; ++i) new_tbl[tbl_off[p] + i] = pages_avail[slot++];
+      }
+    }
+    for (uint32_t p = 0; p < P; ++p)
+      if (cat[p] == ORC_OUT || cat[p] == ORC_DROP_GPU)
+        for (uint32_t i = 0; i < nblk[p]; ++i) new_tbl[tbl_off[p] + i] = ORC_NONE;
+    for (uint64_t j = 0; j < n_free0 + n_rel; ++j) free_map[pages_avail[j]] = (j >= need) ? 1 : 0;
+    memcpy(tbl, new_tbl, sizeof(uint32_t) * tbl_off[P]);
+
+    /* -- step 5b: swap-in into the newly allocated pages -- */
+    if (pool_bytes && host_bufs) {
+      for (uint32_t p = 0; p < P; ++p) {
+        if (cat[p] != ORC_IN) continue;
+        for (uint64_t q = 0; q < planes; ++q)
+          for (uint32_t i = 0; i < nblk[p]; ++i) {
+            uint64_t page = tbl[tbl_off[p] + i];
+            memcpy(pool_bytes + (q * NB + page) * run, host_bufs[p] + (q * nblk[p] + i) * run, run);
+          }
+      }
+    }
+
+    if (summary) {
+      memset(summary, 0, sizeof *summary);
+      summary->m_gpu = m_gpu;
+      summary->m_cpu = m_cpu;
+      for (uint32_t p = 0; p < P; ++p) {
+        uint64_t pages = nblk[p];
+        switch (cat[p]) {
+          case ORC_OUT: summary->n_out++; summary->pages_out += pages; break;
+          case ORC_IN: summary->n_in++; summary->pages_in += pages; break;
+          case ORC_DROP_GPU: summary->n_drop_gpu++; break;
+          case ORC_DROP_CPU: summary->n_drop_cpu++; break;
+          case ORC_ADMIT_GPU: summary->n_admit_gpu++; summary->pages_admit += pages; break;
+          case ORC_ADMIT_CPU: summary->n_admit_cpu++; break;
+          default: break;
+        }
+        if (tier_new[p] == ORC_GPU) summary->gpu_bytes_after += pages * block_bytes;
+        if (tier_new[p] == ORC_CPU) summary->cpu_bytes_after += pages * block_bytes;
+      }
+      summary->pages_free_before = n_free0;
+      summary->pages_released = n_rel;
+      summary->pages_recycled = need > n_free0 ? need - n_free0 : 0;
+      summary->pages_free_after = n_free0 + n_rel - need;
+      summary->bytes_out = summary->pages_out * block_bytes;
+      summary->bytes_in = summary->pages_in * block_bytes;
+    }
+    if (tier_old_out) memcpy(tier_old_out, tier, P);
+    if (category_out) memcpy(category_out, cat, P);
+    if (order_out) memcpy(order_out, order, sizeof(uint32_t) * P);
+    if (rank_out) memcpy(rank_out, rank, sizeof(uint32_t) * P);
+    if (prefix_out) memcpy(prefix_out, prefix, sizeof(uint64_t) * P);
+    memcpy(tier, tier_new, P);
+  }
+
+  free(iota);
+  free(key);
+  free(order);
+  free(rank);
+  free(nblk);
+  free(prefix);
+  free(tier_new);
+  free(cat);
+  free(page_state);
+  free(pages_avail);
+  free(new_tbl);
+  return rc;
+}

@@ -1,0 +1,108 @@
+/*
+ * mori_oracle.h -- plain CPU oracle for MORI's idleness-ranked KV tier placement
+ * (arXiv 2606.00866, "Idleness is Relative").
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may include, link or
+ * call this code; only the tests, the smoke check and the benchmark's CPU
+ * baseline leg use it.  It shares no code, header or constant with the HIP
+ * library: every definition below is restated from the paper on its own.
+ *
+ * What it computes, in the paper's order:
+ *   1. idleness of every program, Eq. 1 (Sec. 4.2), over a window of k cycles;
+ *   2. the relative ranking of all programs by idleness, busiest first
+ *      (Sec. 1 and Sec. 4.3: idleness is relative, programs are ranked);
+ *   3. the capacity-matched boundary: fill the GPU tier from the busiest end of
+ *      the ranking until its byte budget is reached, then the CPU tier the same
+ *      way; the rest waits (Sec. 4.1 three-tier queues, Sec. 4.3, Sec. 7.2);
+ *   4. sticky placement: only programs whose tier changes move (Sec. 4.3), with
+ *      KV pages of paged attention (Sec. 2.1) allocated lowest id first;
+ *   5. the byte movement this implies: demoted programs' pages copied into
+ *      their contiguous host buffers, promoted programs' bytes copied back into
+ *      newly allocated pages (Sec. 4.1: the CPU tier resumes over PCIe).
+ *
+ * Readings where the paper is silent are listed with each function.
+ * Floating point: idleness is computed in IEEE binary32 because it decides an
+ * integer (the ranking) and the GPU path takes that decision in binary32; the
+ * oracle therefore uses the same precision and the same summation order.
+ */
+#ifndef MORI_ORACLE_H
+#define MORI_ORACLE_H
+#include <stdint.h>
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* tiers (Sec. 4.1: GPU queue, CPU queue, Waiting queue) */
+#define ORC_GPU 0u
+#define ORC_CPU 1u
+#define ORC_WAIT 2u
+#define ORC_NONE 0xFFFFFFFFu /* table entry of a block that has no HBM page */
+
+/* flags */
+#define ORC_F_STATUS_KEY 1u     /* Acting programs rank after Reasoning ones (Sec. 4.3.1, demotion) */
+#define ORC_F_SKIP_FIT 2u       /* greedy fit instead of a strict prefix boundary */
+#define ORC_F_IDLENESS_GIVEN 4u /* idleness supplied directly instead of windows */
+
+/* result classes */
+#define ORC_OK 0
+#define ORC_E_INPUT 1  /* malformed program data: windows, idleness, tiers or table offsets */
+#define ORC_E_POOL 2   /* inconsistent page pool: bad/duplicate/leaked/free-but-owned page */
+#define ORC_E_NOSPC 3  /* not enough pages for the promoted programs */
+
+/* transition categories, old tier -> new tier */
+#define ORC_KEPT 0u
+#define ORC_OUT 1u       /* GPU -> CPU: swap-out */
+#define ORC_IN 2u        /* CPU -> GPU: swap-in */
+#define ORC_DROP_GPU 3u  /* GPU -> WAIT: pages released, KV discarded */
+#define ORC_DROP_CPU 4u  /* CPU -> WAIT */
+#define ORC_ADMIT_GPU 5u /* WAIT -> GPU: pages reserved, no copy (prefill recomputes) */
+#define ORC_ADMIT_CPU 6u /* WAIT -> CPU */
+
+typedef struct {
+  uint32_t layers, planes, block_tokens, row_bytes, num_blocks;
+} orc_geometry;
+
+typedef struct {
+  uint32_t m_gpu, m_cpu;
+  uint32_t n_out, n_in, n_drop_gpu, n_drop_cpu, n_admit_gpu, n_admit_cpu;
+  uint64_t pages_out, pages_in, pages_admit;
+  uint64_t pages_free_before, pages_released, pages_recycled, pages_free_after;
+  uint64_t bytes_out, bytes_in, gpu_bytes_after, cpu_bytes_after;
+} orc_summary;
+
+/* Eq. 1 for every program.  window is [P][k][2] (reasoning s, acting s), oldest first. */
+int orc_idleness(uint32_t P, uint32_t k, const float* window, float* iota);
+
+/* 32-bit ranking key from idleness (and status when ORC_F_STATUS_KEY is set). */
+int orc_keys(uint32_t P, const float* iota, const uint8_t* status, uint32_t flags, uint32_t* key);
+
+/* Ascending (key, program id) order; rank is its inverse permutation. */
+void orc_order(uint32_t P, const uint32_t* key, uint32_t* order, uint32_t* rank);
+
+/* Capacity-matched boundary over the ranking.  prefix[r] = KV bytes of the
+ * first r+1 programs in rank order. */
+void orc_boundary(uint32_t P, const uint32_t* order, const uint32_t* nblk, uint64_t block_bytes,
+                  uint64_t gpu_budget, uint64_t cpu_budget, uint32_t flags, uint64_t* prefix,
+                  uint8_t* tier_new, uint32_t* m_gpu, uint32_t* m_cpu);
+
+/* One whole rebalance: Eq. 1 -> ranking -> boundary -> sticky diff -> page
+ * allocation -> table rewrite -> byte movement.  All state arrays are updated
+ * in place only when the result is ORC_OK; on an error nothing is modified.
+ *
+ * pool_bytes [layers*planes][num_blocks][block_tokens*row_bytes] and host_bufs
+ * [P] (one contiguous [layers*planes][nblk_p][block_tokens*row_bytes] buffer per
+ * program) may both be NULL to compute the placement only.
+ * Optional outputs (may be NULL): order, rank, tier_old_out, category, prefix, summary. */
+int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32_t k,
+                  const float* window, const float* iota_given, const uint8_t* status,
+                  const uint32_t* tbl_off, uint32_t tbl_len, uint32_t* tbl, uint8_t* tier,
+                  uint8_t* free_map, uint64_t gpu_budget, uint64_t cpu_budget, uint32_t flags,
+                  uint8_t* const* host_bufs, uint32_t* order, uint32_t* rank, uint8_t* tier_old_out,
+                  uint8_t* category, uint64_t* prefix, orc_summary* summary);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
