@@ -1,0 +1,329 @@
+#!/usr/bin/env python3
+"""Benchmark of the KV tier-migration hot path on one MI355X.
+
+One step = one whole rebalance: Eq. 1 idleness -> ranking -> GPU/CPU/Waiting
+boundaries -> sticky diff and page allocation -> swap-out (GPU -> pinned host)
+concurrently with swap-in (pinned host -> GPU) on two streams.  Steps
+alternate between the drawn idleness windows and the reversed windows (every
+program's reasoning and tool-call times swapped), so each timed step moves
+programs in both directions.
+
+value = KV migration GB/s = (bytes swapped out + bytes swapped in) / step wall
+time, with the pool, tables and windows already resident in HBM and the CPU
+tier already in pinned host memory when the timed region starts.  The
+host-link peak (pinned hipMemcpyAsync, D2H / H2D / both at once) and the HBM
+copy peak are measured in the same run.  The roofline object is for the
+gather/scatter kernel (HBM-bound), timed per launch with events on its stream.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+GIB = 1 << 30
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=6)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="llama3_8b")
+    ap.add_argument("--mode", default="auto", choices=["auto", "kernel", "ce"])
+    ap.add_argument("--arena-gib", type=float, default=60.0, help="pinned CPU-tier arena")
+    ap.add_argument("--cpu-gib", type=float, default=28.0, help="CPU-tier budget")
+    ap.add_argument("--staging-mib", type=int, default=1024)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-verify", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    return ap.parse_args()
+
+
+# --------------------------------------------------------------------------
+# CPU baseline: the oracle, as it stands, on a bounded sample of the workload
+# --------------------------------------------------------------------------
+def cpu_baseline(cfg, cpu_frac: float, seconds: float):
+    import numpy as np
+
+    from oracle import oracle
+    from workload import budget_bytes, fill_pool_np, make_bank, make_instance
+
+    scale = 1.0 / 32
+    inst = make_instance(cfg, scale=scale)
+    g = inst.geom
+    bank = make_bank(cfg.seed, cfg.dtype, g.run_bytes)
+    pool = fill_pool_np(inst, bank)
+    bufs = [np.zeros(int(n) * g.block_bytes, np.uint8) for n in inst.nblk]
+    tbl, tier, free = inst.copy_state()
+    bg = budget_bytes(inst.total_bytes, cfg.gpu_pct)
+    bc = int(inst.total_bytes * cpu_frac)
+    wins = (inst.window, inst.window[:, :, ::-1].copy())
+    moved, spent, steps = 0, 0.0, 0
+    t = 0
+    while True:
+        t0 = time.perf_counter()
+        res = oracle.rebalance(g, window=wins[t % 2], tbl_off=inst.tbl_off, tbl=tbl, tier=tier, free_map=free,
+                               gpu_budget=bg, cpu_budget=bc, pool=pool, host_bufs=bufs)
+        dt = time.perf_counter() - t0
+        assert res.rc == oracle.OK
+        if t >= 1:  # the first step only moves out; time the bidirectional ones
+            moved += res.summary["bytes_out"] + res.summary["bytes_in"]
+            spent += dt
+            steps += 1
+        t += 1
+        if spent >= seconds or t > 200:
+            break
+    return {"value": round(moved / spent / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": (f"{cfg.name} with contexts scaled by {scale:g} ({inst.P} programs, "
+                       f"{inst.total_bytes / GIB:.2f} GiB of KV, same GPU/CPU budget fractions), {steps} "
+                       f"bidirectional rebalances, memcpy per run between host buffers, single thread")}
+
+
+# --------------------------------------------------------------------------
+# peaks measured in the same run
+# --------------------------------------------------------------------------
+def measure_peaks(torch, M, s1, s2):
+    # the HIP runtime torch already loaded (a second copy of the runtime must never be loaded)
+    hip = C.CDLL("libamdhip64.so.7", mode=os.RTLD_NOLOAD | os.RTLD_GLOBAL)
+    hip.hipMemcpyAsync.argtypes = [C.c_void_p, C.c_void_p, C.c_size_t, C.c_int, C.c_void_p]
+    H2D, D2H, D2D = 1, 2, 3
+    n = 4 * GIB
+    dev_a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dev_b = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dev_a.fill_(1)
+    dev_b.fill_(2)
+    rc1, h1 = M.mori_host_alloc(n)
+    rc2, h2 = M.mori_host_alloc(n)
+    assert rc1 == 0 and rc2 == 0
+    C.memset(h1, 3, n)
+    C.memset(h2, 4, n)
+
+    def timed(fn, reps=5):
+        ts = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s1)
+            s2.wait_event(e0)
+            fn()
+            e2 = torch.cuda.Event()
+            e2.record(s2)
+            s1.wait_event(e2)
+            e1.record(s1)
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1) / 1e3)
+        return sorted(ts)[len(ts) // 2]
+
+    def cp(dst, src, kind, s):
+        assert hip.hipMemcpyAsync(dst, src, n, kind, C.c_void_p(s.cuda_stream)) == 0
+
+    t_d2h = timed(lambda: cp(h1, dev_a.data_ptr(), D2H, s1))
+    t_h2d = timed(lambda: cp(dev_b.data_ptr(), h2, H2D, s1))
+    t_bi = timed(lambda: (cp(h1, dev_a.data_ptr(), D2H, s1), cp(dev_b.data_ptr(), h2, H2D, s2)))
+    t_d2d = timed(lambda: cp(dev_b.data_ptr(), dev_a.data_ptr(), D2D, s1))
+    torch.cuda.synchronize()
+    M.mori_host_free(h1)
+    M.mori_host_free(h2)
+    del dev_a, dev_b
+    torch.cuda.empty_cache()
+    return {"d2h_GBps": round(n / t_d2h / 1e9, 2), "h2d_GBps": round(n / t_h2d / 1e9, 2),
+            "bidir_GBps": round(2 * n / t_bi / 1e9, 2), "d2d_copy_GBps": round(2 * n / t_d2d / 1e9, 1),
+            "method": "pinned hipMemcpyAsync, 4 GiB, median of 5 (bidir: D2H and H2D on two streams)"}
+
+
+def main() -> int:
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on exactly one GPU: the KV migration path moves one GPU's pool to its own "
+              "host memory and has no multi-GPU form here (--gpus 1).", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    # The two swap streams are the process's first streams: HIP maps streams to
+    # a small number of hardware queues (4 per process by default) and streams
+    # created later share queues, which serialises swap-out with swap-in.
+    s_out, s_in = torch.cuda.Stream(), torch.cuda.Stream()
+
+    from paper_2606_00866_amd import mori as M
+    from paper_2606_00866_amd.tiering import TierPool
+    from workload import CONFIGS, budget_bytes, fill_pool_torch, make_bank, make_instance, run_content
+
+    cfg = CONFIGS[args.workload]
+    M.lib()
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    inst = make_instance(cfg)
+    g = inst.geom
+    total = inst.total_bytes
+    bg = budget_bytes(total, cfg.gpu_pct)
+    bc = int(args.cpu_gib * GIB)
+    log(f"workload {cfg.name}: P={inst.P} NB={g.num_blocks} block={g.block_bytes} B total={total / GIB:.2f} GiB "
+        f"gpu_budget={bg / GIB:.2f} GiB cpu_budget={bc / GIB:.2f} GiB")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        t0 = time.perf_counter()
+        cpu = cpu_baseline(cfg, bc / total, args.cpu_seconds)
+        log(f"cpu baseline {cpu['value']} GB/s ({time.perf_counter() - t0:.1f} s)")
+
+    peaks = measure_peaks(torch, M, s_out, s_in)
+    log(f"peaks {peaks}")
+
+    free_b, _ = torch.cuda.mem_get_info()
+    need = g.pool_bytes + 2 * args.staging_mib * (1 << 20) + (2 << 30)
+    if free_b < need:
+        raise SystemExit(f"pool needs {need / GIB:.1f} GiB of HBM, {free_b / GIB:.1f} GiB free")
+    t0 = time.perf_counter()
+    pool = torch.empty(g.pool_bytes, dtype=torch.uint8, device="cuda")
+    bank = make_bank(cfg.seed, cfg.dtype, g.run_bytes)
+    bank_dev = torch.from_numpy(bank.view(np.int16)).cuda()
+    fill_pool_torch(pool, inst, bank_dev)
+    torch.cuda.synchronize()
+    log(f"pool {g.pool_bytes / GIB:.2f} GiB filled in {time.perf_counter() - t0:.1f} s")
+    tp = TierPool(g, inst.tbl_off, inst.tbl, inst.tier, inst.free_map, arena_bytes=int(args.arena_gib * GIB),
+                  max_programs=inst.P, staging_bytes=args.staging_mib << 20, pool=pool)
+    mode = {"auto": M.MORI_COPY_AUTO, "kernel": M.MORI_COPY_KERNEL, "ce": M.MORI_COPY_CE}[args.mode]
+    wins = [torch.from_numpy(inst.window).cuda(), torch.from_numpy(inst.window[:, :, ::-1].copy()).cuda()]
+    history = []
+    valid = np.ones(inst.P, bool)  # programs whose KV bytes are defined (never re-admitted from Waiting)
+
+    def one_step(t):
+        p = tp.step(gpu_bytes=bg, cpu_bytes=bc, window=wins[t % 2], mode=mode, s_out=s_out, s_in=s_in)
+        cat = tp.plan_arrays(p)["category"]
+        valid[cat == M.MORI_CAT_ADMIT_GPU] = False
+        valid[cat == M.MORI_CAT_ADMIT_CPU] = False
+        history.append({k: getattr(p, k) for k in ("m_gpu", "m_cpu", "n_out", "n_in", "n_drop_gpu",
+                                                   "n_admit_gpu", "pages_recycled", "bytes_out", "bytes_in")})
+        return p
+
+    for t in range(args.warmup):
+        p = one_step(t)
+        log(f"warmup {t}: out {p.bytes_out / GIB:.2f} GiB in {p.bytes_in / GIB:.2f} GiB")
+    _, last_mode = M.mori_query(tp.ctx, M.MORI_Q_LAST_MODE)
+    M.mori_profile(tp.ctx, True)
+    for d in (0, 1):
+        M.mori_profile_read(tp.ctx, d)
+    torch.cuda.synchronize()
+    moved = 0
+    t_start = time.perf_counter()
+    for t in range(args.warmup, args.warmup + args.steps):
+        p = one_step(t)
+        moved += p.bytes_out + p.bytes_in
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    prof = [M.mori_profile_read(tp.ctx, d) for d in (0, 1)]
+    M.mori_profile(tp.ctx, False)
+    value = moved / elapsed / 1e9
+    log(f"timed {args.steps} steps: {moved / GIB:.2f} GiB in {elapsed:.3f} s -> {value:.2f} GB/s")
+
+    # dominant kernel: the gather/scatter direction with the larger summed kernel time
+    kern = []
+    for d, (rc, n, by, ms) in enumerate(prof):
+        kern.append({"kernel": "swap_kernel<out> (gather)" if d == 0 else "swap_kernel<in> (scatter)",
+                     "launches": n, "payload_bytes": by, "kernel_ms": round(ms, 3),
+                     "avg_launch_ms": round(ms / n, 4) if n else None,
+                     "hbm_GBps": round(2 * by / (ms / 1e3) / 1e9, 1) if ms > 0 else None})
+    dom = max(kern, key=lambda k: k["kernel_ms"])
+    achieved = dom["hbm_GBps"] or 0.0
+
+    verify = None
+    if not args.no_verify:
+        verify = verify_sampled(inst, tp, bank, history, wins, bg, bc, valid, args, M, torch, np, run_content)
+        log(f"verify: {verify}")
+
+    out = {
+        "metric": "KV migration GB/s (D2H+H2D) vs host-link peak; gather/scatter HBM GB/s",
+        "value": round(value, 3),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{cfg.name}: {inst.P} programs, {cfg.layers} layers x {cfg.planes} planes x "
+                         f"{cfg.row_bytes} B rows (8 KV heads x 128 bf16), {cfg.block_tokens}-token blocks, "
+                         f"{g.num_blocks} pages = {g.pool_bytes / GIB:.2f} GiB pool, GPU budget {cfg.gpu_pct}% "
+                         f"of KV bytes, CPU tier {args.cpu_gib:g} GiB in a {args.arena_gib:g} GiB pinned arena; "
+                         f"steps alternate drawn / reversed idleness windows"),
+            "copy_mode": {0: "auto", 1: "kernel", 2: "copy-engine"}[int(last_mode)],
+            "gpu_budget_bytes": bg,
+            "cpu_budget_bytes": bc,
+            "bytes_per_step": int(moved / max(args.steps, 1)),
+        },
+        "hostlink": {**peaks, "frac_of_bidir_peak": round(value / peaks["bidir_GBps"], 4)},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": dom["kernel"], "frac_of_measured_copy_peak":
+                         round(achieved / peaks["d2d_copy_GBps"], 4)},
+        "kernels": kern,
+        "cpu_baseline": cpu,
+        "parity": verify,
+    }
+    print(json.dumps(out), flush=True)
+    tp.close()
+    return 0
+
+
+def verify_sampled(inst, tp, bank, history, wins, bg, bc, valid, args, M, torch, np, run_content):
+    """Full-size parity on sampled outputs: the oracle replays every step's
+    placement from the initial state (tables, tiers, free map compared exactly,
+    per-step summaries compared), and sampled runs of resident programs are
+    compared with the bytes the oracle's copy rule puts there (each run is the
+    input run of the same program, block and plane)."""
+    from oracle import oracle
+
+    g = inst.geom
+    tbl, tier, free = inst.copy_state()
+    wnp = [w.cpu().numpy() for w in wins]
+    for t, h in enumerate(history):
+        res = oracle.rebalance(g, window=wnp[t % 2], tbl_off=inst.tbl_off, tbl=tbl, tier=tier, free_map=free,
+                               gpu_budget=bg, cpu_budget=bc)
+        assert res.rc == oracle.OK
+        for k, v in h.items():
+            if res.summary[k] != v:
+                return {"ok": False, "step": t, "field": k, "gpu": v, "oracle": res.summary[k]}
+    dt, dtier, dfree = tp.state()
+    if not ((dt == tbl).all() and (dtier == tier).all() and (dfree == free).all()):
+        return {"ok": False, "what": "final tables/tiers/free map"}
+    rng = np.random.default_rng(7)
+    checked = 0
+    planes = tp.pool.view(g.nplanes, g.num_blocks, g.run_bytes)
+    for p in np.flatnonzero(valid & (tier != 2) & (inst.nblk > 0)):
+        for _ in range(8):
+            i = int(rng.integers(0, inst.nblk[p]))
+            q = int(rng.integers(0, g.nplanes))
+            expect = run_content(bank, g.run_bytes, p, i, q)[0]
+            if tier[p] == 0:
+                got = planes[q, int(tbl[inst.tbl_off[p] + i])].cpu().numpy()
+            else:
+                hv = tp.host_view(int(p))
+                got = hv[(q * int(inst.nblk[p]) + i) * g.run_bytes:(q * int(inst.nblk[p]) + i + 1) * g.run_bytes]
+            if not np.array_equal(got, expect):
+                return {"ok": False, "what": "bytes", "program": int(p), "block": i, "plane": q}
+            checked += 1
+    return {"ok": True, "steps": len(history), "runs_checked": checked,
+            "programs_checked": int((valid & (tier != 2) & (inst.nblk > 0)).sum())}
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,245 @@
+/*
+ * mori.h -- C ABI of libmori: the MI355X (gfx950) hot path of MORI's
+ * idleness-ranked KV-cache placement (arXiv 2606.00866, "Idleness is
+ * Relative: Exploiting Tool-Call Idle Windows for Offloading in Agentic
+ * Systems with MORI").
+ *
+ * One rebalance of the three-tier placement of Sec. 4.1 (GPU HBM, CPU DRAM,
+ * Waiting), as three calls:
+ *
+ *   mori_rank_partition  Eq. 1 idleness of every program (Sec. 4.2), the
+ *                        relative ranking (Sec. 1, Sec. 4.3), the
+ *                        capacity-matched GPU and CPU boundaries (Sec. 4.1
+ *                        per-tier capacity, Sec. 7.2 fill from the busiest
+ *                        end), the sticky diff (Sec. 4.3: only programs that
+ *                        cross the boundary move), page allocation and the
+ *                        block-table rewrite.
+ *   mori_kv_swap_out     gathers the demoted programs' scattered KV pages into
+ *                        one contiguous buffer per program (GPU -> CPU).
+ *   mori_kv_swap_in      scatters the promoted programs' bytes into the pages
+ *                        allocated for them (CPU -> GPU, Sec. 4.1: a CPU-tier
+ *                        program resumes over PCIe).
+ *
+ * Conventions
+ *   - Every call returns an int: MORI_OK (0) or a negative MORI_E* code.
+ *     Nothing throws across the ABI.  Errors found on the host are reported
+ *     before anything is enqueued and leave all caller memory untouched.
+ *   - Device-side validation (program data, pool consistency, host
+ *     addresses) sets bits of a device error word (MORI_DEV_*).  A plan that
+ *     fails validation modifies no caller memory; its error is returned by
+ *     mori_plan_wait and mori_query.
+ *   - Streams are hipStream_t values passed as void*; NULL is the default
+ *     stream.  The library never synchronises the device.  It blocks the host
+ *     only in mori_plan_wait and in copy-engine swaps (which need the plan).
+ *   - Ownership: the caller owns the pool, the program arrays, the host
+ *     buffers and the streams.  The context owns its device scratch, a small
+ *     pinned mirror of the plan and, for copy-engine swaps, device staging
+ *     buffers, all allocated in mori_create and freed in mori_destroy.
+ *
+ * Layouts
+ *   pool   [layers * planes][num_blocks][block_tokens][row_bytes] bytes in
+ *          HBM.  A "run" is one (plane, page): block_tokens * row_bytes
+ *          contiguous bytes.  A page of a program spans every plane.
+ *   host   one contiguous buffer per CPU-resident program p:
+ *          [layers * planes][nblk_p][block_tokens][row_bytes], so each
+ *          program's runs of one plane are adjacent.
+ *   nblk_p = tbl_off[p+1] - tbl_off[p] whole blocks; a program is never split
+ *          across tiers (Sec. 1: a program sits in exactly one tier at a time).
+ */
+#ifndef MORI_H
+#define MORI_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- return codes ---------------------------------------------------- */
+#define MORI_OK 0
+#define MORI_EINVAL (-1)  /* bad argument: null/misaligned pointer, size, flag or mode */
+#define MORI_ENOSPC (-2)  /* capacity: too many programs, staging too small, registry full */
+#define MORI_ESTATE (-3)  /* call out of order (swap without a plan, swap twice, ...) */
+#define MORI_EHIP (-4)    /* a HIP runtime call failed; mori_query(MORI_Q_LAST_HIP_ERROR) */
+#define MORI_EDEVICE (-5) /* device-side validation failed; see the MORI_DEV_* bits */
+
+/* ---- device error word bits ------------------------------------------- */
+#define MORI_DEV_BAD_WINDOW 0x001u    /* window value negative, NaN or inf, or a total overflowed */
+#define MORI_DEV_BAD_IDLENESS 0x002u  /* given idleness outside [0, 1] */
+#define MORI_DEV_BAD_TIER 0x004u      /* tier value > 2 */
+#define MORI_DEV_BAD_TBL_OFF 0x008u   /* tbl_off not starting at 0, decreasing, or past tbl_len */
+#define MORI_DEV_PAGE_RANGE 0x010u    /* a GPU program's page id >= num_blocks */
+#define MORI_DEV_PAGE_DUP 0x020u      /* a page owned twice, or owned and marked free */
+#define MORI_DEV_PAGE_LEAK 0x040u     /* a page neither free nor owned */
+#define MORI_DEV_NONRES_PAGE 0x080u   /* a CPU/Waiting program's table holds a page */
+#define MORI_DEV_NOSPC 0x100u         /* not enough pages (unreachable for a consistent pool) */
+#define MORI_DEV_HOST_ADDR 0x200u     /* swap address not 16-B aligned or outside registered memory */
+/* classes: program data = 0x00F, pool state = 0x0F0, capacity = 0x100, swap = 0x200 */
+
+/* ---- tiers, table sentinel, flags, copy modes -------------------------- */
+#define MORI_TIER_GPU 0u
+#define MORI_TIER_CPU 1u
+#define MORI_TIER_WAIT 2u
+#define MORI_NO_PAGE 0xFFFFFFFFu
+
+#define MORI_F_STATUS_KEY 1u     /* Acting programs (status 1) rank after all Reasoning ones */
+#define MORI_F_SKIP_FIT 2u       /* greedy fit in rank order instead of a strict prefix */
+#define MORI_F_IDLENESS_GIVEN 4u /* use programs.idleness instead of windows */
+
+#define MORI_COPY_AUTO 0u   /* copy engines (chosen by measurement on MI355X) */
+#define MORI_COPY_KERNEL 1u /* kernels load/store host-mapped memory directly; no host sync */
+#define MORI_COPY_CE 2u     /* kernel gather/scatter through device staging + SDMA copies */
+
+/* transition categories (mori_plan.category) */
+#define MORI_CAT_KEPT 0u
+#define MORI_CAT_OUT 1u       /* GPU -> CPU: bytes gathered to the host */
+#define MORI_CAT_IN 2u        /* CPU -> GPU: bytes scattered into new pages */
+#define MORI_CAT_DROP_GPU 3u  /* GPU -> Waiting: pages released, KV discarded */
+#define MORI_CAT_DROP_CPU 4u  /* CPU -> Waiting */
+#define MORI_CAT_ADMIT_GPU 5u /* Waiting -> GPU: pages reserved, no copy */
+#define MORI_CAT_ADMIT_CPU 6u /* Waiting -> CPU: no copy */
+
+#define MORI_MAX_PROGRAMS 4096u
+#define MORI_MAX_WINDOW 64u
+#define MORI_MAX_RANGES 64u
+
+typedef struct mori_ctx mori_ctx;
+
+/* The paged KV pool in HBM (PagedAttention-style blocks, Sec. 2.1). */
+typedef struct {
+  uint32_t layers;       /* >= 1 */
+  uint32_t planes;       /* >= 1: 2 for K and V, 1 for a compressed latent */
+  uint32_t block_tokens; /* >= 1 tokens per block */
+  uint32_t row_bytes;    /* bytes per token per (layer, plane); multiple of 16 */
+  uint32_t num_blocks;   /* pages in the pool, < 2^32 - 1 */
+  void* base;            /* device pointer, 256-B aligned, layout in the header comment */
+} mori_pool;
+
+/* Per-program state (Sec. 4.1: status, context size and recent durations). */
+typedef struct {
+  uint32_t num_programs;   /* P <= max_programs of the context */
+  uint32_t window_k;       /* cycles per idleness window, 1..MORI_MAX_WINDOW (the paper uses 5) */
+  const float* window;     /* device [P][window_k][2]: (reasoning s, acting s), oldest cycle
+                              first; the newest acting entry is the ongoing call's elapsed time */
+  const float* idleness;   /* device [P]; read only with MORI_F_IDLENESS_GIVEN */
+  const uint8_t* status;   /* device [P] 0 reasoning, 1 acting; read only with MORI_F_STATUS_KEY */
+  const uint32_t* tbl_off; /* device [P+1] CSR offsets into tbl; nblk_p = tbl_off[p+1]-tbl_off[p] */
+  uint32_t tbl_len;        /* entries allocated in tbl (>= tbl_off[P]) */
+  uint32_t* tbl;           /* device [tbl_len], in/out: page id of each logical block of a
+                              GPU-resident program, MORI_NO_PAGE for every other program */
+  uint8_t* tier;           /* device [P], in/out: current tier -> new tier */
+  uint8_t* free_map;       /* device [num_blocks], in/out: 1 = page free */
+} mori_programs;
+
+/* Per-tier capacity (Sec. 4.1: neither tier may exceed its memory). */
+typedef struct {
+  uint64_t gpu_bytes; /* <= num_blocks * block bytes */
+  uint64_t cpu_bytes;
+  uint32_t flags;     /* MORI_F_* */
+} mori_budget;
+
+/* The plan of the last mori_rank_partition, as mirrored on the host.  The
+ * array pointers refer to context-owned pinned memory, valid until the next
+ * mori_rank_partition or mori_destroy. */
+typedef struct {
+  uint32_t num_programs, m_gpu, m_cpu;
+  uint32_t n_out, n_in, n_drop_gpu, n_drop_cpu, n_admit_gpu, n_admit_cpu;
+  uint32_t device_error; /* MORI_DEV_* bits; 0 when the plan is valid */
+  uint64_t pages_out, pages_in, pages_admit;
+  uint64_t pages_free_before, pages_released, pages_recycled, pages_free_after;
+  uint64_t bytes_out, bytes_in, gpu_bytes_after, cpu_bytes_after;
+  const uint32_t* order;        /* [P] program ids, busiest first */
+  const uint64_t* prefix;       /* [P] inclusive KV-byte prefix in rank order */
+  const uint8_t* tier_old;      /* [P] */
+  const uint8_t* tier_new;      /* [P] */
+  const uint8_t* category;      /* [P] MORI_CAT_* */
+  const uint32_t* out_programs; /* [n_out] in rank order */
+  const uint32_t* in_programs;  /* [n_in] in rank order */
+} mori_plan;
+
+/* ---- context ----------------------------------------------------------- */
+
+/* Creates a context for one pool on the current HIP device.  max_programs <=
+ * MORI_MAX_PROGRAMS bounds P of every later call.  staging_bytes is the
+ * device staging buffer of copy-engine swaps, per direction (0: 512 MiB; it
+ * is rounded down to whole runs and must hold at least one); copy-engine
+ * swaps move the bytes in chunks of that size.  *out is set on success.
+ * EINVAL: null pool/out, bad geometry or alignment; EHIP: allocation. */
+int mori_create(const mori_pool* pool, uint32_t max_programs, uint64_t staging_bytes, mori_ctx** out);
+
+/* Waits for the context's outstanding work and frees it.  NULL is a no-op. */
+int mori_destroy(mori_ctx* ctx);
+
+/* Registers a range that swap buffers may live in: pinned host memory from
+ * hipHostMalloc / mori_host_alloc (used through its device mapping), or
+ * device memory (then swaps are device-to-device gathers and scatters).  The
+ * swap kernels touch no address outside registered ranges.  EINVAL: null,
+ * zero size, or memory HIP does not know; ENOSPC: MORI_MAX_RANGES reached. */
+int mori_register(mori_ctx* ctx, void* ptr, uint64_t bytes);
+
+/* Pinned, device-mapped host memory for the CPU tier (hipHostMalloc with the
+ * mapped and portable flags), and its release. */
+int mori_host_alloc(uint64_t bytes, void** out);
+int mori_host_free(void* ptr);
+
+/* ---- the hot path ------------------------------------------------------ */
+
+/* Computes the new placement and rewrites tbl, tier and free_map in stream
+ * order.  Waits (on the stream) for the previous plan's swaps.  The plan is
+ * copied to the context's pinned mirror; read it with mori_plan_wait.
+ * EINVAL: null pointers, P > max_programs, window_k out of range, unknown
+ * flags, gpu_bytes > num_blocks * block bytes. */
+int mori_rank_partition(mori_ctx* ctx, const mori_programs* programs, const mori_budget* budget,
+                        void* stream);
+
+/* Blocks the host until the last plan is on the host and fills *out.
+ * Returns MORI_EDEVICE (with out->device_error set) if the plan was rejected
+ * on the device, ESTATE if there is no plan. */
+int mori_plan_wait(mori_ctx* ctx, mori_plan* out);
+
+/* Swap-out of the last plan: for every program p with category OUT, copies
+ * each run (plane q, logical block i) from its old page to
+ * host_dst[p] + (q * nblk_p + i) * run_bytes.  host_dst is a host array of P
+ * addresses (read during the call; entries of other programs are ignored),
+ * each 16-B aligned inside a registered range with room for nblk_p * block
+ * bytes.  Pages released by these programs may be reused only after this
+ * swap completes.  ESTATE: no plan, or swap-out already enqueued for it. */
+int mori_kv_swap_out(mori_ctx* ctx, const uint64_t* host_dst, uint32_t mode, void* stream);
+
+/* Swap-in of the last plan: for every program p with category IN, copies
+ * host_src[p] + (q * nblk_p + i) * run_bytes into its newly allocated page of
+ * block i, plane q.  Waits (on the stream) for the plan and, before writing a
+ * page released by a swap-out of the same plan, for that swap-out.  The host
+ * buffers may be reused after it completes.  ESTATE: no plan, swap-in already
+ * enqueued, or swap-out of the plan not yet enqueued. */
+int mori_kv_swap_in(mori_ctx* ctx, const uint64_t* host_src, uint32_t mode, void* stream);
+
+/* ---- introspection ----------------------------------------------------- */
+#define MORI_Q_LAST_HIP_ERROR 1 /* last hipError_t seen by the context */
+#define MORI_Q_DEVICE_ERROR 2   /* device error word of the last plan and swaps (waits for them) */
+#define MORI_Q_LAST_MODE 3      /* copy mode actually used by the last swap */
+#define MORI_Q_PLAN_EVENT 4     /* hipEvent_t recorded when the plan is complete */
+#define MORI_Q_OUT_EVENT 5      /* hipEvent_t recorded when the last swap-out is complete */
+#define MORI_Q_IN_EVENT 6       /* hipEvent_t recorded when the last swap-in is complete */
+int mori_query(mori_ctx* ctx, int what, uint64_t* value);
+
+/* Static description of a return code. */
+const char* mori_strerror(int code);
+
+/* ---- kernel timing ------------------------------------------------------ */
+/* With profiling on, every gather/scatter kernel launch of the swaps is
+ * bracketed by timing events recorded on the stream it is launched on (up to
+ * 4096 launches per direction between reads).  mori_profile_read waits for
+ * those events and returns, for direction 0 (swap-out) or 1 (swap-in), the
+ * number of launches, the payload bytes they moved and their summed duration
+ * in milliseconds, then clears the record.  EINVAL: null pointers or a bad
+ * direction; ENOSPC (from a swap) is never raised: launches beyond the record
+ * capacity are simply not timed. */
+int mori_profile(mori_ctx* ctx, int enable);
+int mori_profile_read(mori_ctx* ctx, int direction, uint64_t* launches, uint64_t* payload_bytes,
+                      double* kernel_ms);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MORI_H */

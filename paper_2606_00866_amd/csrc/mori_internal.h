@@ -1,0 +1,107 @@
+// Internal declarations of libmori shared by the kernel files and the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/mori.h"
+
+namespace mori {
+
+// Page-state bits of the page-allocation pass.
+constexpr uint32_t PS_FREE = 1u;   // marked free in the caller's free map before the step
+constexpr uint32_t PS_OWNED = 2u;  // owned by a GPU-resident program
+constexpr uint32_t PS_REL = 4u;    // owned by a program leaving the GPU this step
+
+constexpr int PAGE_TILE = 4096;    // pages per workgroup in the page-allocation kernels
+constexpr int PAGE_WG = 256;       // threads per page-allocation workgroup (16 pages each)
+
+// Plan summary as kept on the device (the head of the plan blob copied to the host).
+struct DevSummary {
+  uint32_t num_programs, m_gpu, m_cpu;
+  uint32_t n_out, n_in, n_drop_gpu, n_drop_cpu, n_admit_gpu, n_admit_cpu;
+  uint32_t error;
+  uint64_t pages_out, pages_in, pages_admit;
+  uint64_t pages_free_before, pages_released, pages_recycled, pages_free_after;
+  uint64_t bytes_out, bytes_in, gpu_bytes_after, cpu_bytes_after;
+  uint64_t need;  // pages_in + pages_admit
+};
+
+// A registered memory range usable by the swap kernels.
+struct DevRange {
+  uint64_t host_base;  // address as the caller names it
+  uint64_t bytes;
+  uint64_t dev_base;   // the same memory as the GPU addresses it
+  uint64_t is_device;  // 1: HBM, 0: pinned host memory
+};
+
+// Everything the plan kernels read and write.
+struct PlanArgs {
+  // caller-owned
+  const float* window;
+  const float* idleness;
+  const uint8_t* status;
+  const uint32_t* tbl_off;
+  uint32_t* tbl;
+  uint8_t* tier;
+  uint8_t* free_map;
+  uint32_t tbl_len, P, k, flags, NB, ntiles;
+  uint64_t block_bytes, gpu_bytes, cpu_bytes;
+  // context scratch: plan blob (mirrored to the host)
+  DevSummary* sum;
+  uint32_t* order;
+  uint64_t* prefix;
+  uint8_t* tier_old;
+  uint8_t* tier_new;
+  uint8_t* cat;
+  uint32_t* out_prog;
+  uint32_t* in_prog;
+  uint32_t* out_pg_base;  // [n_out + 1] first out-page index of each out program
+  uint32_t* in_pg_base;   // [n_in + 1] first slot of each in program
+  // context scratch: device only
+  uint32_t* base;         // per program: out-page base (OUT) or slot base (IN, ADMIT_GPU)
+  uint32_t* pstate;       // [NB]
+  uint32_t* out_src;      // [pages_out] old page of each out page index
+  uint32_t* in_dst;       // [need] page of each slot
+  uint64_t* tile_cnt;     // [ntiles] packed (free-before count, released count << 32)
+  uint64_t* tile_base;    // [ntiles] exclusive prefix of tile_cnt
+  uint32_t* swap_err;     // cleared by every plan
+};
+
+// Everything a swap kernel reads.
+struct SwapArgs {
+  uint8_t* pool;
+  uint64_t NB, run;
+  uint32_t LC;              // layers * planes
+  const DevSummary* sum;
+  const uint32_t* prog;     // out_prog or in_prog
+  const uint32_t* pg_base;  // out_pg_base or in_pg_base
+  const uint32_t* pages;    // out_src (by out-page index) or in_dst (by slot)
+  const uint64_t* addr;     // device address of each program's host buffer
+  const uint32_t* swap_err;
+  uint8_t* staging;         // non-null: chunk staging buffer (copy-engine mode)
+  uint64_t u_begin, u_end;  // staging mode: unit range of the chunk
+  uint32_t part;            // swap-in: 0 all slots, 1 slots < free-before, 2 slots >= free-before
+};
+
+struct TranslateArgs {
+  const DevSummary* sum;
+  const uint32_t* prog;     // out_prog or in_prog (count n_out / n_in)
+  int dir_in;               // 0 out, 1 in
+  const uint32_t* tbl_off;
+  uint64_t block_bytes;
+  const uint64_t* addr_in;  // [P] caller addresses (copied to the device)
+  uint64_t* addr_out;       // [P] translated device addresses
+  const DevRange* ranges;
+  uint32_t nranges;
+  uint32_t* swap_err;
+};
+
+// launchers (return the launch error)
+hipError_t launch_rank(const PlanArgs& a, hipStream_t s);
+hipError_t launch_pages(const PlanArgs& a, hipStream_t s);
+hipError_t launch_translate(const TranslateArgs& a, hipStream_t s);
+hipError_t launch_swap_out(const SwapArgs& a, uint32_t grid, hipStream_t s);
+hipError_t launch_swap_in(const SwapArgs& a, uint32_t grid, hipStream_t s);
+
+}  // namespace mori

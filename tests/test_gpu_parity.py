@@ -1,0 +1,204 @@
+"""GPU parity: libmori (through the C ABI) against the CPU oracle, element by
+element -- rank order, prefix, categories, summary, block tables, tiers, free
+map and every resident byte -- on seeded inputs, in both copy modes."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import Pair, log
+from oracle import oracle
+from paper_2606_00866_amd import mori as M
+from paper_2606_00866_amd.tiering import MoriError
+from workload import TINY, Geometry, budget_bytes, make_instance, random_instance
+
+pytestmark = pytest.mark.gpu
+
+MODES = [M.MORI_COPY_KERNEL, M.MORI_COPY_CE]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    assert torch.cuda.is_available(), "GPU tests need the MI355X"
+    M.lib()
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_tiny_rebalance_round_trip_reversal(mode):
+    inst = make_instance(TINY)
+    log(f"tiny mode={mode} P={inst.P} NB={inst.geom.num_blocks}")
+    pair = Pair(inst, seed=TINY.seed)
+    try:
+        bg = budget_bytes(inst.total_bytes, TINY.gpu_pct)
+        res, plan = pair.step(gpu_bytes=bg, cpu_bytes=inst.total_bytes, window=inst.window, mode=mode)
+        assert plan.n_out > 0 and plan.bytes_out > 0
+        rev = inst.window[:, :, ::-1].copy()
+        res, plan = pair.step(gpu_bytes=bg, cpu_bytes=inst.total_bytes, window=rev, mode=mode)
+        assert plan.n_in > 0 and plan.n_out > 0
+        res, plan = pair.step(gpu_bytes=bg, cpu_bytes=inst.total_bytes, window=inst.window, mode=mode)
+        assert plan.n_in > 0
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("seed", range(48))
+def test_random_instances(seed):
+    rng = np.random.default_rng(1000 + seed)
+    inst = random_instance(rng, P=int(rng.integers(0, 40)), max_blocks=int(rng.choice([3, 12, 40])),
+                           ties=bool(seed % 2))
+    mode = MODES[seed % 2]
+    flags = [0, M.MORI_F_SKIP_FIT, M.MORI_F_STATUS_KEY, 0][seed % 4]
+    log(f"random seed={seed} P={inst.P} NB={inst.geom.num_blocks} geom={inst.geom} mode={mode} flags={flags}")
+    pair = Pair(inst, seed=seed)
+    try:
+        bb = inst.geom.block_bytes
+        for step in range(3):
+            bg = int(rng.integers(0, inst.geom.num_blocks + 1)) * bb
+            bc = int(rng.integers(0, inst.total_bytes // max(bb, 1) + 2)) * bb
+            w = inst.window if step != 1 else inst.window[:, :, ::-1].copy()
+            pair.step(gpu_bytes=bg, cpu_bytes=bc, window=w, status=inst.status, flags=flags, mode=mode)
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_recycled_pages_worked_example_b(mode):
+    """Example B of the plan fixture (one recycled page): the swap-in must not
+    overwrite page 1 before the swap-out has read it."""
+    geom = Geometry(layers=3, planes=2, block_tokens=4, row_bytes=256, num_blocks=6)
+    inst = random_instance(np.random.default_rng(0), P=3, geom=geom, extra_free=0)
+    inst.nblk[:] = [2, 2, 3]
+    inst.tbl_off[:] = [0, 2, 4, 7]
+    inst.tbl = np.array([3, 1, 0, 4, 0xFFFFFFFF, 0xFFFFFFFF, 0xFFFFFFFF], np.uint32)
+    inst.tier = np.array([0, 0, 1], np.uint8)
+    inst.free_map = np.array([0, 0, 1, 0, 0, 1], np.uint8)
+    inst.geom = geom
+    pair = Pair(inst, seed=5)
+    try:
+        res, plan = pair.step(gpu_bytes=5 * geom.block_bytes, cpu_bytes=2 * geom.block_bytes,
+                              iota=np.array([0.875, 0.125, 0.25], np.float32), flags=M.MORI_F_IDLENESS_GIVEN,
+                              mode=mode)
+        assert res.rc == oracle.OK and plan.pages_recycled == 1
+    finally:
+        pair.close()
+
+
+def test_edge_cases_empty_and_degenerate():
+    geom = Geometry(layers=1, planes=2, block_tokens=2, row_bytes=32, num_blocks=16)
+    rng = np.random.default_rng(7)
+    cases = [
+        random_instance(rng, P=0, geom=geom, extra_free=4),                    # no programs
+        random_instance(rng, P=1, geom=geom, extra_free=0),                    # one program
+        random_instance(rng, P=9, max_blocks=0, geom=geom, extra_free=3),      # all zero-block programs
+        random_instance(rng, P=12, geom=geom, extra_free=0, tier_p=(1.0, 0, 0)),  # pool exactly full
+    ]
+    for inst in cases:
+        log(f"edge P={inst.P} NB={inst.geom.num_blocks}")
+        if inst.geom.num_blocks == 0:
+            continue
+        pair = Pair(inst, seed=3)
+        try:
+            bb = inst.geom.block_bytes
+            for bg in (0, inst.geom.num_blocks * bb):  # empty GPU budget, then the whole pool
+                for bc in (0, inst.total_bytes):
+                    pair.step(gpu_bytes=bg, cpu_bytes=bc, window=inst.window, mode=M.MORI_COPY_CE)
+        finally:
+            pair.close()
+
+
+@pytest.mark.parametrize("k", [1, 5, 64])
+def test_window_lengths_and_max_programs(k):
+    """P = 4096 (the maximum) with ties, and windows of 1, 5 and 64 cycles."""
+    rng = np.random.default_rng(k)
+    P = 4096
+    geom = Geometry(layers=1, planes=1, block_tokens=1, row_bytes=16, num_blocks=0)
+    inst = random_instance(rng, P=P, max_blocks=2, geom=geom, ties=True)
+    vals = np.array([0.0, 0.5, 1.0, 2.0], np.float32)
+    inst.window = vals[rng.integers(0, 4, size=(P, k, 2))]
+    log(f"max programs k={k} NB={inst.geom.num_blocks}")
+    pair = Pair(inst, seed=k)
+    try:
+        bb = inst.geom.block_bytes
+        pair.step(gpu_bytes=inst.geom.num_blocks * bb // 2, cpu_bytes=inst.total_bytes // 3, window=inst.window,
+                  mode=M.MORI_COPY_KERNEL)
+    finally:
+        pair.close()
+
+
+def test_device_validation_rejects_and_leaves_state():
+    rng = np.random.default_rng(21)
+    inst = random_instance(rng, P=10, extra_free=4, tier_p=(0.6, 0.3, 0.1))
+    pair = Pair(inst, seed=1)
+    try:
+        bb = inst.geom.block_bytes
+        before = pair.tp.state()
+        bad = inst.window.copy()
+        bad[3, 2, 1] = np.nan
+        w = torch.from_numpy(bad).cuda()
+        rc = pair.tp.rank_partition(gpu_bytes=bb, cpu_bytes=bb, window=w)
+        assert rc == M.MORI_OK
+        rc, plan = pair.tp.plan_wait()
+        assert rc == M.MORI_EDEVICE and plan.device_error & M.MORI_DEV_BAD_WINDOW
+        after = pair.tp.state()
+        assert all((a == b).all() for a, b in zip(before, after))
+        # an inconsistent pool: a free page that a GPU program also owns
+        gpu_progs = [p for p in range(inst.P) if inst.tier[p] == 0 and inst.nblk[p] > 0]
+        pg = int(inst.tbl[inst.tbl_off[gpu_progs[0]]])
+        pair.tp.free_map[pg] = 1
+        rc = pair.tp.rank_partition(gpu_bytes=bb, cpu_bytes=bb, window=torch.from_numpy(inst.window).cuda())
+        rc, plan = pair.tp.plan_wait()
+        assert rc == M.MORI_EDEVICE and plan.device_error & M.MORI_DEV_PAGE_DUP
+        pair.tp.free_map[pg] = 0
+        # swap without a fresh plan after a rejected one: swaps do nothing and report the error
+        assert pair.tp.swap_out(M.MORI_COPY_KERNEL) == M.MORI_OK
+        torch.cuda.synchronize()
+        rc, err = M.mori_query(pair.tp.ctx, M.MORI_Q_DEVICE_ERROR)
+        assert rc == 0 and err & M.MORI_DEV_PAGE_DUP
+    finally:
+        pair.close()
+
+
+def test_host_side_state_errors():
+    inst = make_instance(TINY)
+    pair = Pair(inst, seed=1)
+    try:
+        tp = pair.tp
+        assert tp.swap_out() == M.MORI_ESTATE  # no plan yet
+        assert tp.rank_partition(gpu_bytes=inst.geom.num_blocks * inst.geom.block_bytes + 1, cpu_bytes=0,
+                                 window=torch.from_numpy(inst.window).cuda()) == M.MORI_EINVAL
+        w = torch.from_numpy(inst.window).cuda()
+        assert tp.rank_partition(gpu_bytes=0, cpu_bytes=inst.total_bytes, window=w, flags=64) == M.MORI_EINVAL
+        assert tp.rank_partition(gpu_bytes=0, cpu_bytes=inst.total_bytes, window=w) == M.MORI_OK
+        rc, plan = tp.plan_wait()
+        assert rc == 0
+        tp.place_host_buffers()
+        assert tp.swap_in() == M.MORI_ESTATE       # swap-out must be enqueued first
+        assert tp.swap_out(mode=7) == M.MORI_EINVAL
+        # a destination outside every registered range is refused before anything is enqueued
+        saved = tp.host_addr.copy()
+        tp.host_addr[plan.out_programs[0]] = 0x1000
+        assert tp.swap_out(M.MORI_COPY_CE) == M.MORI_EINVAL
+        tp.host_addr[:] = saved
+        assert tp.swap_out(M.MORI_COPY_CE) == M.MORI_OK
+        assert tp.swap_out(M.MORI_COPY_CE) == M.MORI_ESTATE  # once per plan
+        assert tp.swap_in(M.MORI_COPY_CE) == M.MORI_OK
+        tp.synchronize()
+    finally:
+        pair.close()
+
+
+def test_kernel_mode_bad_address_is_caught_on_device():
+    inst = make_instance(TINY)
+    pair = Pair(inst, seed=1)
+    try:
+        tp = pair.tp
+        w = torch.from_numpy(inst.window).cuda()
+        assert tp.rank_partition(gpu_bytes=0, cpu_bytes=inst.total_bytes, window=w) == M.MORI_OK
+        rc, plan = tp.plan_wait()
+        tp.place_host_buffers()
+        tp.host_addr[plan.out_programs[0]] += 8  # misaligned
+        assert tp.swap_out(M.MORI_COPY_KERNEL) == M.MORI_OK
+        torch.cuda.synchronize()
+        rc, err = M.mori_query(tp.ctx, M.MORI_Q_DEVICE_ERROR)
+        assert err & M.MORI_DEV_HOST_ADDR
+    finally:
+        pair.close()

@@ -1,7 +1,7 @@
 """Seeded synthetic inputs shared by the oracle and the HIP path.
 
 This module draws inputs only -- program sizes, idleness windows, block tables,
-pool occupancy, budgets, KV bytes and host-buffer extents -- and holds none of
+pool occupancy, budgets and KV bytes -- and holds none of
 the placement method's arithmetic (no idleness, ranking, boundary, page
 allocation or copying).  Every draw is reproducible from the config's seed:
 ``SeedSequence(seed).spawn`` gives one independent stream per draw kind, taken
@@ -347,45 +347,3 @@ def fill_pool_torch(pool, inst: Instance, bank_dev, owner_p=None, owner_i=None, 
             tags = run_tag(pp, ii, q)
             vals.view(torch.int32)[:, 0] = torch.where(tags >= 2**31, tags - 2**32, tags).to(torch.int32)
             dst[pages] = vals
-
-
-# --------------------------------------------------------------------------
-# host buffers: first-fit extents in one pinned arena
-# --------------------------------------------------------------------------
-class FirstFitArena:
-    """First-fit allocator of byte extents inside one host arena (the CPU tier's
-    memory).  Offsets are multiples of ``align``."""
-
-    def __init__(self, capacity: int, align: int = 4096):
-        self.capacity = capacity
-        self.align = align
-        self.free = [(0, capacity)]  # sorted (start, length)
-        self.used = {}
-
-    def alloc(self, size: int):
-        size = max(self.align, (size + self.align - 1) // self.align * self.align)
-        for j, (s, n) in enumerate(self.free):
-            if n >= size:
-                if n == size:
-                    self.free.pop(j)
-                else:
-                    self.free[j] = (s + size, n - size)
-                self.used[s] = size
-                return s
-        return None
-
-    def release(self, off: int):
-        size = self.used.pop(off)
-        self.free.append((off, size))
-        self.free.sort()
-        merged = []
-        for s, n in self.free:
-            if merged and merged[-1][0] + merged[-1][1] == s:
-                merged[-1] = (merged[-1][0], merged[-1][1] + n)
-            else:
-                merged.append((s, n))
-        self.free = merged
-
-    @property
-    def bytes_used(self) -> int:
-        return sum(self.used.values())
