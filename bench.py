@@ -144,6 +144,25 @@ def measure_peaks(torch, M, s1, s2):
             "method": "pinned hipMemcpyAsync, 4 GiB, median of 5 (bidir: D2H and H2D on two streams)"}
 
 
+def stored_traffic(workload: str, direction: int):
+    """HBM bytes per launch of the swap kernel from the committed counter
+    summary, or None when that summary is for another workload or the kernel
+    source has changed since the counters were taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", f"swap_kernel_{workload}_pmc.md")
+    if not os.path.exists(path):
+        return None
+    line = [l for l in open(path) if l.startswith("traffic_json: ")]
+    if not line:
+        return None
+    rec = json.loads(line[0][len("traffic_json: "):])
+    src = os.path.join(ROOT, "paper_2606_00866_amd", "csrc", "swap_kernels.hip")
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["kernel_source_sha256"]:
+        return None
+    return rec["gather" if direction == 0 else "scatter"]["traffic_bytes_per_launch"]
+
+
 def main() -> int:
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -161,7 +180,7 @@ def main() -> int:
     s_out, s_in = torch.cuda.Stream(), torch.cuda.Stream()
 
     from paper_2606_00866_amd import mori as M
-    from paper_2606_00866_amd.tiering import TierPool
+    from paper_2606_00866_amd.tiering import TierPool, check
     from workload import CONFIGS, budget_bytes, fill_pool_torch, make_bank, make_instance, run_content
 
     cfg = CONFIGS[args.workload]
@@ -202,8 +221,24 @@ def main() -> int:
     history = []
     valid = np.ones(inst.P, bool)  # programs whose KV bytes are defined (never re-admitted from Waiting)
 
-    def one_step(t):
-        p = tp.step(gpu_bytes=bg, cpu_bytes=bc, window=wins[t % 2], mode=mode, s_out=s_out, s_in=s_in)
+    span = [0.0, 0.0]  # summed device time from the step's start to the end of swap-out / swap-in
+
+    def one_step(t, timed=False):
+        e0, e_out, e_in = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        e0.record(s_out)
+        check(tp.rank_partition(gpu_bytes=bg, cpu_bytes=bc, window=wins[t % 2], stream=s_out), "rank")
+        rc, p = tp.plan_wait()
+        if rc != M.MORI_OK:
+            raise RuntimeError(f"plan rejected: {rc} {p.device_error:#x}")
+        tp.place_host_buffers()
+        check(tp.swap_out(mode, s_out), "swap_out")
+        e_out.record(s_out)
+        check(tp.swap_in(mode, s_in), "swap_in")
+        e_in.record(s_in)
+        tp.synchronize()
+        if timed:
+            span[0] += e0.elapsed_time(e_out)
+            span[1] += e0.elapsed_time(e_in)
         cat = tp.plan_arrays(p)["category"]
         valid[cat == M.MORI_CAT_ADMIT_GPU] = False
         valid[cat == M.MORI_CAT_ADMIT_CPU] = False
@@ -222,7 +257,7 @@ def main() -> int:
     moved = 0
     t_start = time.perf_counter()
     for t in range(args.warmup, args.warmup + args.steps):
-        p = one_step(t)
+        p = one_step(t, timed=True)
         moved += p.bytes_out + p.bytes_in
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
@@ -231,14 +266,16 @@ def main() -> int:
     value = moved / elapsed / 1e9
     log(f"timed {args.steps} steps: {moved / GIB:.2f} GiB in {elapsed:.3f} s -> {value:.2f} GB/s")
 
-    # dominant kernel: the gather/scatter direction with the larger summed kernel time
+    # dominant kernel: the gather/scatter kernel of the direction on the step's
+    # critical path (the direction whose work ends last)
     kern = []
     for d, (rc, n, by, ms) in enumerate(prof):
         kern.append({"kernel": "swap_kernel<out> (gather)" if d == 0 else "swap_kernel<in> (scatter)",
                      "launches": n, "payload_bytes": by, "kernel_ms": round(ms, 3),
                      "avg_launch_ms": round(ms / n, 4) if n else None,
                      "hbm_GBps": round(2 * by / (ms / 1e3) / 1e9, 1) if ms > 0 else None})
-    dom = max(kern, key=lambda k: k["kernel_ms"])
+    crit = 0 if span[0] >= span[1] else 1
+    dom = kern[crit]
     achieved = dom["hbm_GBps"] or 0.0
 
     verify = None
@@ -272,10 +309,12 @@ def main() -> int:
         },
         "hostlink": {**peaks, "frac_of_bidir_peak": round(value / peaks["bidir_GBps"], 4)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": stored_traffic(cfg.name, crit),
+                     "algorithmic_bytes_per_launch": int(2 * dom["payload_bytes"] / max(dom["launches"], 1)),
                      "kernel": dom["kernel"], "frac_of_measured_copy_peak":
                          round(achieved / peaks["d2d_copy_GBps"], 4)},
         "kernels": kern,
+        "direction_ms_per_step": {"swap_out": round(span[0] / args.steps, 2), "swap_in": round(span[1] / args.steps, 2)},
         "cpu_baseline": cpu,
         "parity": verify,
     }
