@@ -1,0 +1,185 @@
+"""The named workloads on the GPU, in the launch configuration bench.py times
+(copy-engine swaps, 1 GiB staging per direction, one pinned CPU-tier arena).
+
+Full-size Llama-3-8B, Llama-3-70B and MLA pools (136-155 GiB of HBM): the oracle
+replays every step's placement and the per-step summaries, final block tables,
+tiers and free map must match exactly; every resident run's tag is checked and
+sampled runs are compared byte for byte with their content-addressed value.
+
+Churn (1024 programs, 100 steps, GPU budget swinging 45-65%, 10% of programs
+flipping phase per step), scaled to fit one GPU and the pinned-memory ceiling:
+placement and summary compared with the oracle after every step.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import log
+from oracle import oracle
+from paper_2606_00866_amd import mori as M
+from paper_2606_00866_amd.tiering import TierPool
+from workload import (CHURN, LLAMA3_70B, LLAMA3_8B, MLA, budget_bytes, churn_steps, fill_pool_torch, make_bank,
+                      make_instance, program_content_torch, run_content, run_tag)
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+GIB = 1 << 30
+SUMMARY = ("m_gpu", "m_cpu", "n_out", "n_in", "n_drop_gpu", "n_drop_cpu", "n_admit_gpu", "n_admit_cpu", "pages_out",
+           "pages_in", "pages_admit", "pages_free_before", "pages_released", "pages_recycled", "pages_free_after",
+           "bytes_out", "bytes_in", "gpu_bytes_after", "cpu_bytes_after")
+
+
+class Harness:
+    def __init__(self, inst, arena_bytes, staging=1 << 30, fill=True):
+        self.inst = inst
+        g = inst.geom
+        self.g = g
+        free, _ = torch.cuda.mem_get_info()
+        assert g.pool_bytes + 4 * GIB < free, f"pool {g.pool_bytes / GIB:.1f} GiB > free {free / GIB:.1f} GiB"
+        self.bank = make_bank(inst.seed, inst.dtype, g.run_bytes)
+        self.bank_dev = torch.from_numpy(self.bank.view(np.int16)).cuda()
+        pool = torch.empty(g.pool_bytes, dtype=torch.uint8, device="cuda")
+        if fill:
+            fill_pool_torch(pool, inst, self.bank_dev)
+        self.tp = TierPool(g, inst.tbl_off, inst.tbl, inst.tier, inst.free_map, arena_bytes=arena_bytes,
+                           max_programs=inst.P, staging_bytes=staging, pool=pool)
+        self.tbl, self.tier, self.free = inst.copy_state()
+        self.valid = np.ones(inst.P, bool)
+        self.s_out, self.s_in = torch.cuda.Stream(), torch.cuda.Stream()
+        self.steps = 0
+
+    def close(self):
+        torch.cuda.synchronize()
+        self.tp.close()
+        del self.tp.pool
+        torch.cuda.empty_cache()
+
+    def step(self, window, bg, bc, mode=M.MORI_COPY_AUTO, iota=None):
+        inst = self.inst
+        flags = oracle.F_IDLENESS_GIVEN if iota is not None else 0
+        res = oracle.rebalance(self.g, window=window, iota=iota, tbl_off=inst.tbl_off, tbl=self.tbl, tier=self.tier,
+                               free_map=self.free, gpu_budget=bg, cpu_budget=bc, flags=flags)
+        assert res.rc == oracle.OK
+        w = None if window is None else torch.from_numpy(np.ascontiguousarray(window)).cuda()
+        it = None if iota is None else torch.from_numpy(np.ascontiguousarray(iota, np.float32)).cuda()
+        plan = self.tp.step(gpu_bytes=bg, cpu_bytes=bc, window=w, idleness=it, flags=flags, mode=mode,
+                            s_out=self.s_out, s_in=self.s_in)
+        for k in SUMMARY:
+            assert getattr(plan, k) == res.summary[k], (self.steps, k, getattr(plan, k), res.summary[k])
+        arr = self.tp.plan_arrays(plan)
+        assert (arr["order"] == res.order).all() and (arr["category"] == res.category).all()
+        tbl, tier, free = self.tp.state()
+        assert (tbl == self.tbl).all() and (tier == self.tier).all() and (free == self.free).all(), self.steps
+        self.prefill(res.category)
+        self.steps += 1
+        return plan
+
+    def prefill(self, cat):
+        """Programs admitted from Waiting get their KV recomputed (an engine's
+        prefill in a real system); the harness writes the expected content."""
+        inst, g = self.inst, self.g
+        adm_g = np.flatnonzero((cat == oracle.ADMIT_GPU) & (inst.nblk > 0))
+        if adm_g.size:
+            op = np.zeros(g.num_blocks, np.int64)
+            oi = np.zeros(g.num_blocks, np.int64)
+            for p in adm_g:
+                pages_p = self.tbl[inst.tbl_off[p]:inst.tbl_off[p + 1]].astype(np.int64)
+                op[pages_p] = p
+                oi[pages_p] = np.arange(pages_p.size)
+            pages = np.concatenate([self.tbl[inst.tbl_off[p]:inst.tbl_off[p + 1]] for p in adm_g]).astype(np.int64)
+            fill_pool_torch(self.tp.pool, inst, self.bank_dev, torch.from_numpy(op).cuda(),
+                            torch.from_numpy(oi).cuda(), pages=torch.from_numpy(pages).cuda())
+        for p in np.flatnonzero((cat == oracle.ADMIT_CPU) & (inst.nblk > 0)):
+            dst = torch.from_numpy(self.tp.host_view(int(p)).view(np.int16))
+            dst.copy_(program_content_torch(inst, self.bank_dev, int(p)).cpu())
+        torch.cuda.synchronize()
+
+    def check_tags(self):
+        """The tag of every run of every resident program sits where the tables
+        (GPU) or the program's host buffer (CPU) say."""
+        inst, g = self.inst, self.g
+        planes = self.tp.pool.view(torch.int32).view(g.nplanes, g.num_blocks, g.run_bytes // 4)
+        for p in range(inst.P):
+            n = int(inst.nblk[p])
+            if n == 0 or self.tier[p] == 2:
+                continue
+            q = np.repeat(np.arange(g.nplanes), n)
+            i = np.tile(np.arange(n), g.nplanes)
+            want = run_tag(np.full(q.size, p, np.int64), i.astype(np.int64), q.astype(np.int64)).astype(np.uint32)
+            if self.tier[p] == 0:
+                pages = torch.from_numpy(self.tbl[inst.tbl_off[p]:inst.tbl_off[p + 1]].astype(np.int64)).cuda()
+                got = planes[:, pages, 0].reshape(-1).cpu().numpy().view(np.uint32)
+            else:
+                got = self.tp.host_view(p).view(np.uint32).reshape(g.nplanes * n, g.run_bytes // 4)[:, 0]
+            assert (got == want).all(), ("tag", p, int(self.tier[p]))
+
+    def check_bytes(self, per_program=4, seed=0):
+        inst, g = self.inst, self.g
+        rng = np.random.default_rng(seed)
+        planes = self.tp.pool.view(g.nplanes, g.num_blocks, g.run_bytes)
+        n_checked = 0
+        for p in np.flatnonzero((self.tier != 2) & (inst.nblk > 0)):
+            n = int(inst.nblk[p])
+            for _ in range(per_program):
+                i, q = int(rng.integers(0, n)), int(rng.integers(0, g.nplanes))
+                expect = run_content(self.bank, g.run_bytes, p, i, q)[0]
+                if self.tier[p] == 0:
+                    got = planes[q, int(self.tbl[inst.tbl_off[p] + i])].cpu().numpy()
+                else:
+                    got = self.tp.host_view(int(p))[(q * n + i) * g.run_bytes:(q * n + i + 1) * g.run_bytes]
+                assert np.array_equal(got, expect), ("bytes", int(p), i, q)
+                n_checked += 1
+        return n_checked
+
+
+@pytest.mark.parametrize("cfg", [LLAMA3_8B, LLAMA3_70B, MLA], ids=lambda c: c.name)
+def test_full_size_workload(cfg):
+    inst = make_instance(cfg)
+    total = inst.total_bytes
+    bg = budget_bytes(total, cfg.gpu_pct)
+    bc = 28 * GIB
+    log(f"{cfg.name}: P={inst.P} NB={inst.geom.num_blocks} pool {inst.geom.pool_bytes / GIB:.1f} GiB "
+        f"gpu {bg / GIB:.1f} GiB cpu {bc / GIB:.1f} GiB")
+    h = Harness(inst, arena_bytes=60 * GIB)
+    try:
+        wins = (inst.window, inst.window[:, :, ::-1].copy())
+        for t in range(3):
+            if t < 2:  # drawn windows, then every program's reasoning and tool time swapped
+                plan = h.step(wins[t], bg, bc)
+            else:  # given idleness: CPU-tier programs busiest, then GPU-tier ones, Waiting last
+                iota = np.array([0.5, 0.1, 0.9], np.float32)[h.tier]  # indexed by tier: GPU, CPU, Wait
+                plan = h.step(None, bg, bc, iota=iota)
+            log(f"  step {t}: out {plan.bytes_out / GIB:.2f} GiB in {plan.bytes_in / GIB:.2f} GiB "
+                f"admit {plan.n_admit_gpu} drop {plan.n_drop_gpu} recycled {plan.pages_recycled}")
+        assert plan.n_in > 0 and plan.n_out > 0
+        h.check_tags()
+        log(f"  sampled runs checked: {h.check_bytes()}")
+    finally:
+        h.close()
+
+
+def test_churn_scaled():
+    """Churn at 8% of its context lengths (about 46 GiB of KV, a 30 GiB pool and
+    a CPU tier of a quarter of the KV bytes): 100 steps, both directions each step."""
+    scale = 0.08
+    inst = make_instance(CHURN, scale=scale, resident="wait")
+    total = inst.total_bytes
+    bc = total // 4
+    log(f"churn x{scale}: P={inst.P} NB={inst.geom.num_blocks} total {total / GIB:.1f} GiB cpu {bc / GIB:.1f} GiB")
+    h = Harness(inst, arena_bytes=int(2.2 * bc) + GIB, fill=False)
+    try:
+        h.step(inst.window, budget_bytes(total, CHURN.pct_swing[0]), bc)  # step 0: place everything
+        moved, recycled_steps = 0, 0
+        for t, pct, busy, window in churn_steps(CHURN, inst.busy):
+            mode = M.MORI_COPY_CE if t % 2 else M.MORI_COPY_KERNEL  # both copy modes at scale
+            plan = h.step(window, budget_bytes(total, pct), bc, mode=mode)
+            moved += plan.bytes_out + plan.bytes_in
+            recycled_steps += plan.pages_recycled > 0
+            if t % 20 == 0:
+                log(f"  step {t}: pct {pct:.1f} out {plan.bytes_out / GIB:.2f} in {plan.bytes_in / GIB:.2f} GiB "
+                    f"recycled {plan.pages_recycled}")
+                h.check_bytes(per_program=1, seed=t)
+        assert moved > 0
+        assert recycled_steps > 0  # swap-ins onto pages released by the same step's swap-out
+        h.check_tags()
+    finally:
+        h.close()

@@ -347,3 +347,26 @@ def fill_pool_torch(pool, inst: Instance, bank_dev, owner_p=None, owner_i=None, 
             tags = run_tag(pp, ii, q)
             vals.view(torch.int32)[:, 0] = torch.where(tags >= 2**31, tags - 2**32, tags).to(torch.int32)
             dst[pages] = vals
+
+
+def program_content_torch(inst: Instance, bank_dev, p: int, out=None):
+    """Program p's KV in the host layout [planes][nblk][run], generated on the
+    device (int16 tensor of nblk * block / 2 elements, written into ``out`` when given)."""
+    import torch
+
+    g = inst.geom
+    n = int(inst.nblk[p])
+    e = g.run_bytes // 2
+    dev = bank_dev.device
+    q = torch.arange(g.nplanes, device=dev, dtype=torch.int64).repeat_interleave(n)
+    i = torch.arange(n, device=dev, dtype=torch.int64).repeat(g.nplanes)
+    pp = torch.full_like(q, p)
+    win = torch.as_strided(bank_dev, (BANK, e), (1, 1))
+    vals = torch.index_select(win, 0, run_offset(pp, i, q))
+    tags = run_tag(pp, i, q)
+    vals.view(torch.int32)[:, 0] = torch.where(tags >= 2**31, tags - 2**32, tags).to(torch.int32)
+    vals = vals.reshape(-1)
+    if out is not None:
+        out.copy_(vals)
+        return out
+    return vals
