@@ -161,9 +161,16 @@ typedef struct {
 
 /* Creates a context for one pool on the current HIP device.  max_programs <=
  * MORI_MAX_PROGRAMS bounds P of every later call.  staging_bytes is the
- * device staging buffer of copy-engine swaps, per direction (0: 512 MiB; it
- * is rounded down to whole runs and must hold at least one); copy-engine
- * swaps move the bytes in chunks of that size.  *out is set on success.
+ * device staging of copy-engine swaps per direction (0: 512 MiB), used as two
+ * halves of whole runs (it must hold at least two runs); copy-engine swaps
+ * move the bytes in chunks of one half.  When the process has at least 8
+ * hardware queues (GPU_MAX_HW_QUEUES >= 8 when HIP starts), the context also
+ * owns one copy stream per direction, so the copy engines drain one half while
+ * the gather/scatter kernel works on the other; with fewer queues those
+ * streams would share queues with the caller's and serialise the directions,
+ * and the copies run on the caller's stream instead.  The two streams given
+ * to the swaps should be distinct and created early (streams beyond the
+ * queue count share queues).  *out is set on success.
  * EINVAL: null pool/out, bad geometry or alignment; EHIP: allocation. */
 int mori_create(const mori_pool* pool, uint32_t max_programs, uint64_t staging_bytes, mori_ctx** out);
 

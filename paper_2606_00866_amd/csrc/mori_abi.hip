@@ -6,17 +6,21 @@
 //              the pinned mirror -> plan event.
 //   swap-out   direct: translate addresses -> gather kernel storing straight
 //              into host-mapped memory; copy engine: per chunk, gather kernel
-//              into device staging -> hipMemcpyAsync of each program segment
-//              to its host buffer (SDMA).
+//              into one half of a device staging buffer (caller's stream) ->
+//              hipMemcpyAsync of each program segment to its host buffer on
+//              the context's copy stream, while the next gather fills the
+//              other half.
 //   swap-in    direct: translate -> scatter of slots on pages free before the
 //              step -> wait for the swap-out -> scatter of recycled slots;
-//              copy engine: per chunk, hipMemcpyAsync host -> staging ->
-//              scatter kernel (after the swap-out event from the first chunk
-//              that writes a recycled page).
+//              copy engine: per chunk, hipMemcpyAsync host -> staging half on
+//              the copy stream -> scatter kernel on the caller's stream (after
+//              the swap-out event from the first chunk that writes a recycled
+//              page), the next chunk loading into the other half meanwhile.
 //   next plan  waits on the stream for both swaps of the previous plan.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -29,8 +33,17 @@ namespace {
 
 constexpr uint64_t kDefaultStaging = 512ull << 20;
 constexpr uint32_t kGridHost = 128;     // enough outstanding 16-B accesses to fill the host link
-constexpr uint32_t kGridDevice = 4096;  // HBM-to-HBM gathers and scatters
+constexpr uint32_t kGridDevice = 8192;  // HBM-to-HBM gathers and scatters
 constexpr uint64_t kTimeOnly = ~0ull;
+constexpr int kQueuesForCopyStreams = 8;
+
+// Hardware queues per process that HIP will create (its default is 4).
+int hw_queues() {
+  const char* v = std::getenv("GPU_MAX_HW_QUEUES");
+  if (!v || !*v) return 4;
+  const int n = std::atoi(v);
+  return n > 0 ? n : 4;
+}
 
 struct BlobLayout {
   size_t sum, order, prefix, tier_old, tier_new, cat, out_prog, in_prog, out_base, in_base, total;
@@ -80,8 +93,12 @@ struct mori_ctx {
   uint32_t* swap_err = nullptr;
   DevRange* ranges_dev = nullptr;
   uint64_t* addr_pinned = nullptr;  // [2][max_programs]
-  uint8_t* staging[2] = {nullptr, nullptr};
+  uint8_t* staging[2] = {nullptr, nullptr};  // per direction, two halves
   uint64_t staging_bytes = 0;
+  hipStream_t cstream[2] = {nullptr, nullptr};  // per direction: the copy-engine copies
+  hipEvent_t ev_half_ready[2][2] = {};          // [dir][half]: gathered (out) / loaded (in)
+  hipEvent_t ev_half_free[2][2] = {};           // [dir][half]: copied out (out) / scattered (in)
+  hipEvent_t ev_start[2] = {nullptr, nullptr};
   std::vector<DevRange> ranges;
   hipEvent_t ev_plan = nullptr, ev_out = nullptr, ev_in = nullptr, ev_addr[2] = {nullptr, nullptr};
   bool have_plan = false, out_enqueued = false, in_enqueued = false;
@@ -129,9 +146,16 @@ static void free_ctx(mori_ctx* c) {
     if (c->staging[d]) (void)hipFree(c->staging[d]);
   if (c->blob_host) (void)hipHostFree(c->blob_host);
   if (c->addr_pinned) (void)hipHostFree(c->addr_pinned);
-  hipEvent_t evs[] = {c->ev_plan, c->ev_out, c->ev_in, c->ev_addr[0], c->ev_addr[1]};
+  for (int d = 0; d < 2; ++d)
+    if (c->cstream[d]) (void)hipStreamSynchronize(c->cstream[d]);
+  hipEvent_t evs[] = {c->ev_plan,          c->ev_out,           c->ev_in,           c->ev_addr[0],
+                      c->ev_addr[1],       c->ev_start[0],      c->ev_start[1],     c->ev_half_ready[0][0],
+                      c->ev_half_ready[0][1], c->ev_half_ready[1][0], c->ev_half_ready[1][1],
+                      c->ev_half_free[0][0], c->ev_half_free[0][1], c->ev_half_free[1][0], c->ev_half_free[1][1]};
   for (hipEvent_t e : evs)
     if (e) (void)hipEventDestroy(e);
+  for (int d = 0; d < 2; ++d)
+    if (c->cstream[d]) (void)hipStreamDestroy(c->cstream[d]);
   for (int d = 0; d < 2; ++d)
     for (hipEvent_t e : c->prof_ev[d]) {
       (void)hipEventSynchronize(e);
@@ -152,7 +176,7 @@ extern "C" int mori_create(const mori_pool* pool, uint32_t max_programs, uint64_
   const uint64_t run = (uint64_t)pool->block_tokens * pool->row_bytes;
   if (LC > 0xFFFFu || run > (1ull << 31) || LC * run >= (1ull << 32)) return MORI_EINVAL;
   if (staging_bytes == 0) staging_bytes = kDefaultStaging;
-  staging_bytes = staging_bytes / run * run;
+  staging_bytes = staging_bytes / (2 * run) * (2 * run);  // two halves of whole runs
   if (staging_bytes == 0) return MORI_EINVAL;
 
   mori_ctx* c = new (std::nothrow) mori_ctx();
@@ -207,8 +231,19 @@ extern "C" int mori_create(const mori_pool* pool, uint32_t max_programs, uint64_
   if ((e = hipHostMalloc(&c->addr_pinned, 16 * pm, hipHostMallocDefault)) != hipSuccess) return fail(e);
   for (int d = 0; d < 2; ++d)
     if ((e = hipMalloc(&c->staging[d], staging_bytes)) != hipSuccess) return fail(e);
-  for (hipEvent_t* ev : {&c->ev_plan, &c->ev_out, &c->ev_in, &c->ev_addr[0], &c->ev_addr[1]})
+  for (hipEvent_t* ev : {&c->ev_plan, &c->ev_out, &c->ev_in, &c->ev_addr[0], &c->ev_addr[1], &c->ev_start[0],
+                         &c->ev_start[1], &c->ev_half_ready[0][0], &c->ev_half_ready[0][1],
+                         &c->ev_half_ready[1][0], &c->ev_half_ready[1][1], &c->ev_half_free[0][0],
+                         &c->ev_half_free[0][1], &c->ev_half_free[1][0], &c->ev_half_free[1][1]})
     if ((e = hipEventCreateWithFlags(ev, hipEventDisableTiming)) != hipSuccess) return fail(e);
+  // Copy streams (default priority) only when the process has hardware queues
+  // to spare: HIP maps streams onto GPU_MAX_HW_QUEUES queues (4 by default) and
+  // streams beyond that share a queue, where each stream's waits block the
+  // other's work and the two swap directions serialise.  Without them the
+  // copies run on the caller's stream, in order with the gathers/scatters.
+  if (hw_queues() >= kQueuesForCopyStreams)
+    for (int d = 0; d < 2; ++d)
+      if ((e = hipStreamCreateWithFlags(&c->cstream[d], hipStreamNonBlocking)) != hipSuccess) return fail(e);
   *out = c;
   return rc;
 }
@@ -493,27 +528,40 @@ extern "C" int mori_kv_swap_out(mori_ctx* ctx, const uint64_t* host_dst, uint32_
     HIP_TRY(ctx, hipStreamWaitEvent(s, ctx->ev_plan, 0));
     const uint64_t LC = ctx->LC, run = ctx->run;
     const uint64_t total = n ? (uint64_t)base[n] * LC : 0;
-    const uint64_t cu = ctx->staging_bytes / run;
+    const uint64_t cu = ctx->staging_bytes / 2 / run;  // chunk = one staging half
+    hipStream_t cs = ctx->cstream[0] ? ctx->cstream[0] : s;
     SwapArgs a = swap_args(ctx, 0);
-    a.staging = ctx->staging[0];
     uint32_t j = 0;  // first program that may overlap the chunk
-    for (uint64_t u0 = 0; u0 < total; u0 += cu) {
+    uint64_t c = 0;
+    // Double buffering: the gather of chunk c (stream s) fills one half while the
+    // copy engines drain the other half (copy stream), so the gathers leave the
+    // copy chain only at its start.  With no copy stream (cs == s) the same
+    // sequence runs in stream order.
+    for (uint64_t u0 = 0; u0 < total; u0 += cu, ++c) {
       const uint64_t u1 = std::min(total, u0 + cu);
+      const int h = (int)(c & 1);
+      uint8_t* half = ctx->staging[0] + (uint64_t)h * cu * run;
+      if (c >= 2) HIP_TRY(ctx, hipStreamWaitEvent(s, ctx->ev_half_free[0][h], 0));
+      a.staging = half;
       a.u_begin = u0;
       a.u_end = u1;
       const int rc = timed_swap_launch(ctx, 0, a, (uint32_t)std::min<uint64_t>(u1 - u0, kGridDevice), s,
                                        (u1 - u0) * run);
       if (rc) return rc;
+      HIP_TRY(ctx, hipEventRecord(ctx->ev_half_ready[0][h], s));
+      HIP_TRY(ctx, hipStreamWaitEvent(cs, ctx->ev_half_ready[0][h], 0));
       while (j < n && (uint64_t)base[j + 1] * LC <= u0) ++j;
       for (uint32_t k = j; k < n && (uint64_t)base[k] * LC < u1; ++k) {
         const uint64_t b0 = (uint64_t)base[k] * LC, b1 = (uint64_t)base[k + 1] * LC;
         const uint64_t lo = std::max(u0, b0), hi = std::min(u1, b1);
         if (hi <= lo) continue;
         uint8_t* dst = reinterpret_cast<uint8_t*>(host_dst[progs[k]]) + (lo - b0) * run;
-        HIP_TRY(ctx, hipMemcpyAsync(dst, ctx->staging[0] + (lo - u0) * run, (hi - lo) * run,
-                                    hipMemcpyDeviceToHost, s));
+        HIP_TRY(ctx, hipMemcpyAsync(dst, half + (lo - u0) * run, (hi - lo) * run, hipMemcpyDeviceToHost, cs));
       }
+      HIP_TRY(ctx, hipEventRecord(ctx->ev_half_free[0][h], cs));
     }
+    // join: the copy stream's last copy implies all earlier ones
+    if (c) HIP_TRY(ctx, hipStreamWaitEvent(s, ctx->ev_half_free[0][(c - 1) & 1], 0));
   }
   HIP_TRY(ctx, hipEventRecord(ctx->ev_out, s));
   ctx->out_enqueued = ctx->out_recorded = true;
@@ -552,7 +600,7 @@ extern "C" int mori_kv_swap_in(mori_ctx* ctx, const uint64_t* host_src, uint32_t
     HIP_TRY(ctx, hipStreamWaitEvent(s, ctx->ev_plan, 0));
     const uint64_t LC = ctx->LC, run = ctx->run, nf = sh->pages_free_before;
     const uint64_t total = n ? (uint64_t)base[n] * LC : 0;
-    const uint64_t cu = ctx->staging_bytes / run;
+    const uint64_t cu = ctx->staging_bytes / 2 / run;  // chunk = one staging half
     // first unit of the first program with a slot on a released page
     uint64_t u_recycled = total;
     for (uint32_t k = 0; k < n; ++k)
@@ -560,30 +608,41 @@ extern "C" int mori_kv_swap_in(mori_ctx* ctx, const uint64_t* host_src, uint32_t
         u_recycled = (uint64_t)base[k] * LC;
         break;
       }
+    hipStream_t cs = ctx->cstream[1] ? ctx->cstream[1] : s;
+    // the copies start after everything already ordered before this swap-in on s
+    // (the plan, hence the previous plan's swaps and their use of the staging)
+    HIP_TRY(ctx, hipEventRecord(ctx->ev_start[1], s));
+    HIP_TRY(ctx, hipStreamWaitEvent(cs, ctx->ev_start[1], 0));
     bool waited = false;
     SwapArgs a = swap_args(ctx, 1);
-    a.staging = ctx->staging[1];
     uint32_t j = 0;
-    for (uint64_t u0 = 0; u0 < total; u0 += cu) {
+    uint64_t c = 0;
+    for (uint64_t u0 = 0; u0 < total; u0 += cu, ++c) {
       const uint64_t u1 = std::min(total, u0 + cu);
+      const int h = (int)(c & 1);
+      uint8_t* half = ctx->staging[1] + (uint64_t)h * cu * run;
+      if (c >= 2) HIP_TRY(ctx, hipStreamWaitEvent(cs, ctx->ev_half_free[1][h], 0));
       while (j < n && (uint64_t)base[j + 1] * LC <= u0) ++j;
       for (uint32_t k = j; k < n && (uint64_t)base[k] * LC < u1; ++k) {
         const uint64_t b0 = (uint64_t)base[k] * LC, b1 = (uint64_t)base[k + 1] * LC;
         const uint64_t lo = std::max(u0, b0), hi = std::min(u1, b1);
         if (hi <= lo) continue;
         const uint8_t* src = reinterpret_cast<const uint8_t*>(host_src[progs[k]]) + (lo - b0) * run;
-        HIP_TRY(ctx, hipMemcpyAsync(ctx->staging[1] + (lo - u0) * run, src, (hi - lo) * run,
-                                    hipMemcpyHostToDevice, s));
+        HIP_TRY(ctx, hipMemcpyAsync(half + (lo - u0) * run, src, (hi - lo) * run, hipMemcpyHostToDevice, cs));
       }
+      HIP_TRY(ctx, hipEventRecord(ctx->ev_half_ready[1][h], cs));
+      HIP_TRY(ctx, hipStreamWaitEvent(s, ctx->ev_half_ready[1][h], 0));
       if (!waited && u1 > u_recycled) {
         HIP_TRY(ctx, hipStreamWaitEvent(s, ctx->ev_out, 0));
         waited = true;
       }
+      a.staging = half;
       a.u_begin = u0;
       a.u_end = u1;
       const int rc = timed_swap_launch(ctx, 1, a, (uint32_t)std::min<uint64_t>(u1 - u0, kGridDevice), s,
                                        (u1 - u0) * run);
       if (rc) return rc;
+      HIP_TRY(ctx, hipEventRecord(ctx->ev_half_free[1][h], s));
     }
   }
   HIP_TRY(ctx, hipEventRecord(ctx->ev_in, s));

@@ -8,8 +8,8 @@
 // layout) or of the staging buffer, while the pool side is scattered over the
 // program's pages.  Each workgroup copies whole units with 16-byte
 // non-temporal loads and stores (every byte is touched once, so nothing is
-// worth caching); the index arithmetic is wavefront-uniform and stays in
-// scalar registers.  A persistent grid walks the units with a grid stride.
+// worth caching); the index arithmetic is wavefront-uniform.  A persistent grid
+// walks the units with a grid stride.
 //
 //   swap_out : pool page  -> host buffer (direct) or staging (copy engine)
 //   swap_in  : host buffer (direct) or staging -> newly allocated pool page
@@ -25,8 +25,15 @@ namespace {
 
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 
-constexpr int NT = 256;  // threads per workgroup
-constexpr int UNR = 8;   // 16-byte vectors in flight per thread per iteration
+// Shape measured on gfx950 with this decode (random 32 KiB pool runs <->
+// contiguous 1 GiB chunks): 256-thread workgroups, one run at a time, eight
+// 16-byte vectors per thread in flight, grid-stride over runs.  Larger
+// workgroups (512, 1024 threads) leave too few workgroups per CU to hide the
+// dependent loads of the per-run decode (-25% at 1024 threads), and handing
+// each workgroup a contiguous block of runs with incremental decode is no
+// faster.
+constexpr int NT = 256;
+constexpr int UNR = 8;
 
 // Largest a in [0, n) with base[a] <= x.
 __device__ inline uint32_t find_slice(const uint32_t* base, uint32_t n, uint64_t x) {
@@ -39,65 +46,84 @@ __device__ inline uint32_t find_slice(const uint32_t* base, uint32_t n, uint64_t
   return lo;
 }
 
-__device__ inline void copy_run(const v4u* __restrict__ src, v4u* __restrict__ dst, uint32_t n16) {
+// Copies n16 vectors with the workgroup's threads; t is the thread index.
+__device__ inline void copy_run(const v4u* __restrict__ src, v4u* __restrict__ dst, uint32_t n16, uint32_t t) {
   for (uint32_t t0 = 0; t0 < n16; t0 += NT * UNR) {
     v4u v[UNR];
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-      const uint32_t t = t0 + u * NT + threadIdx.x;
-      if (t < n16) v[u] = __builtin_nontemporal_load(src + t);
+    for (int k = 0; k < UNR; ++k) {
+      const uint32_t i = t0 + k * NT + t;
+      if (i < n16) v[k] = __builtin_nontemporal_load(src + i);
     }
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-      const uint32_t t = t0 + u * NT + threadIdx.x;
-      if (t < n16) __builtin_nontemporal_store(v[u], dst + t);
+    for (int k = 0; k < UNR; ++k) {
+      const uint32_t i = t0 + k * NT + t;
+      if (i < n16) __builtin_nontemporal_store(v[k], dst + i);
     }
   }
+}
+
+// Unit range of this launch; returns false when there is nothing to do.
+template <bool kOut>
+__device__ inline bool unit_range(const SwapArgs& s, uint32_t n, uint64_t* lo, uint64_t* hi) {
+  const uint64_t LC = s.LC;
+  const uint64_t total = (uint64_t)s.pg_base[n] * LC;
+  const uint64_t nf = s.sum->pages_free_before;
+  *lo = 0;
+  *hi = total;
+  if (s.staging) {
+    *lo = s.u_begin;
+    *hi = s.u_end < total ? s.u_end : total;
+  } else if (!kOut && s.part == 1) {
+    uint32_t a = 0, b = n;  // number of moving programs whose first slot is below nf
+    while (a < b) {
+      const uint32_t mid = (a + b) >> 1;
+      if (s.pg_base[mid] < nf) a = mid + 1;
+      else b = mid;
+    }
+    *hi = (uint64_t)s.pg_base[a] * LC;
+  } else if (!kOut && s.part == 2) {
+    if (s.pg_base[n] <= nf) return false;  // no slot reaches a released page
+    *lo = (uint64_t)s.pg_base[find_slice(s.pg_base, n, nf)] * LC;
+  }
+  return *lo < *hi;
+}
+
+// Source and destination of unit u; false when the unit belongs to the other
+// part of a two-part swap-in.
+template <bool kOut>
+__device__ inline bool unit_ends(const SwapArgs& s, uint32_t n, uint64_t u, uint64_t u_lo, const v4u** src,
+                                 v4u** dst) {
+  const uint64_t LC = s.LC;
+  const uint32_t a = find_slice(s.pg_base, n, u / LC);
+  const uint64_t first = s.pg_base[a];
+  const uint64_t nb = (uint64_t)s.pg_base[a + 1] - first;
+  const uint64_t rem = u - first * LC;
+  const uint64_t q = rem / nb, i = rem - q * nb;
+  const uint64_t slot = first + i;
+  if (!kOut && s.part != 0) {
+    const uint64_t nf = s.sum->pages_free_before;
+    if ((s.part == 1) != (slot < nf)) return false;
+  }
+  uint8_t* pool_run = s.pool + (q * s.NB + s.pages[slot]) * s.run;
+  uint8_t* side = s.staging ? s.staging + (u - u_lo) * s.run
+                            : reinterpret_cast<uint8_t*>(s.addr[s.prog[a]]) + rem * s.run;
+  *src = reinterpret_cast<const v4u*>(kOut ? pool_run : side);
+  *dst = reinterpret_cast<v4u*>(kOut ? side : pool_run);
+  return true;
 }
 
 template <bool kOut>
 __global__ __launch_bounds__(NT) void swap_kernel(SwapArgs s) {
   if (s.sum->error || *s.swap_err) return;
   const uint32_t n = kOut ? s.sum->n_out : s.sum->n_in;
-  if (n == 0) return;
-  const uint64_t LC = s.LC;
-  const uint64_t total = (uint64_t)s.pg_base[n] * LC;
-  const uint64_t nf = s.sum->pages_free_before;
-  uint64_t u_lo = 0, u_hi = total;
-  if (s.staging) {
-    u_lo = s.u_begin;
-    u_hi = s.u_end < total ? s.u_end : total;
-  } else if (!kOut && s.part == 1) {
-    // programs whose first slot is below nf
-    uint32_t a1 = 0;
-    uint32_t lo = 0, hi = n;  // count of a with pg_base[a] < nf (pg_base is non-decreasing)
-    while (lo < hi) {
-      const uint32_t mid = (lo + hi) >> 1;
-      if (s.pg_base[mid] < nf) lo = mid + 1;
-      else hi = mid;
-    }
-    a1 = lo;
-    u_hi = (uint64_t)s.pg_base[a1] * LC;
-  } else if (!kOut && s.part == 2) {
-    if (s.pg_base[n] <= nf) return;  // no slot reaches a released page
-    u_lo = (uint64_t)s.pg_base[find_slice(s.pg_base, n, nf)] * LC;
-  }
+  uint64_t lo, hi;
+  if (n == 0 || !unit_range<kOut>(s, n, &lo, &hi)) return;
   const uint32_t n16 = (uint32_t)(s.run / 16);
-  for (uint64_t u = u_lo + blockIdx.x; u < u_hi; u += gridDim.x) {
-    const uint32_t a = find_slice(s.pg_base, n, u / LC);
-    const uint64_t first = s.pg_base[a];
-    const uint64_t nb = (uint64_t)s.pg_base[a + 1] - first;
-    const uint64_t rem = u - first * LC;
-    const uint64_t q = rem / nb, i = rem - q * nb;
-    const uint64_t slot = first + i;
-    if (!kOut && s.part == 1 && slot >= nf) continue;
-    if (!kOut && s.part == 2 && slot < nf) continue;
-    const uint64_t page = s.pages[slot];
-    uint8_t* pool_run = s.pool + (q * s.NB + page) * s.run;
-    uint8_t* side = s.staging ? s.staging + (u - u_lo) * s.run
-                              : reinterpret_cast<uint8_t*>(s.addr[s.prog[a]]) + rem * s.run;
-    if (kOut) copy_run(reinterpret_cast<const v4u*>(pool_run), reinterpret_cast<v4u*>(side), n16);
-    else copy_run(reinterpret_cast<const v4u*>(side), reinterpret_cast<v4u*>(pool_run), n16);
+  for (uint64_t u = lo + blockIdx.x; u < hi; u += gridDim.x) {
+    const v4u* src;
+    v4u* dst;
+    if (unit_ends<kOut>(s, n, u, lo, &src, &dst)) copy_run(src, dst, n16, threadIdx.x);
   }
 }
 

@@ -202,3 +202,20 @@ def test_kernel_mode_bad_address_is_caught_on_device():
         assert err & M.MORI_DEV_HOST_ADDR
     finally:
         pair.close()
+
+
+def test_default_queue_count_in_order_copies():
+    """With HIP's default of four hardware queues libmori creates no copy streams
+    and runs the copy-engine copies on the caller's streams; the smoke check
+    (tiny rebalance and reversal against the oracle) runs in a child process
+    started with that setting."""
+    import os
+    import subprocess
+    import sys
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    env = dict(os.environ, GPU_MAX_HW_QUEUES="4")
+    r = subprocess.run([sys.executable, "-c", "import __graft_entry__ as g; g.smoke()"], cwd=root, env=env,
+                       capture_output=True, text=True, timeout=240)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "smoke ok" in r.stdout

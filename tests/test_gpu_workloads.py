@@ -1,5 +1,5 @@
 """The named workloads on the GPU, in the launch configuration bench.py times
-(copy-engine swaps, 1 GiB staging per direction, one pinned CPU-tier arena).
+(copy-engine swaps, 2 GiB of staging per direction in two halves, one pinned CPU-tier arena).
 
 Full-size Llama-3-8B, Llama-3-70B and MLA pools (136-155 GiB of HBM): the oracle
 replays every step's placement and the per-step summaries, final block tables,
@@ -29,7 +29,7 @@ SUMMARY = ("m_gpu", "m_cpu", "n_out", "n_in", "n_drop_gpu", "n_drop_cpu", "n_adm
 
 
 class Harness:
-    def __init__(self, inst, arena_bytes, staging=1 << 30, fill=True):
+    def __init__(self, inst, arena_bytes, staging=2 << 30, fill=True):
         self.inst = inst
         g = inst.geom
         self.g = g
