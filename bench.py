@@ -59,6 +59,7 @@ def parse():
     ap.add_argument("--staging-mib", type=int, default=2048, help="per direction, two halves")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-verify", action="store_true")
+    ap.add_argument("--no-evict", action="store_true", help="skip the typed eviction-order leg")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--hw-queues", type=int, default=8, help="GPU_MAX_HW_QUEUES for this process (read at start)")
     return ap.parse_args()
@@ -183,6 +184,49 @@ def measure_peaks(torch, M, s1, s2):
                        "together on two streams, 8 GiB over the time both took.  bidir: the larger of that and the "
                        "concurrent capacity (overlapped rate of the direction that ended first plus the overlapped "
                        "rate of the other, its tail after the first ended taken at its one-direction rate)")}
+
+
+def evict_leg(torch, np, M, sizes, reps=20):
+    """Typed eviction order (Sec. 4.3.2) on synthetic block metadata: device
+    time per call (events on its stream, median of `reps`), the oracle's time
+    for the same input, and exact parity of order, prefix and count."""
+    from oracle import oracle
+    from workload import eviction_blocks
+
+    out = []
+    for N in sizes:
+        rng = np.random.default_rng(N)
+        typ, la, size = eviction_blocks(rng, N, programs=1024, tie_frac=0.5, var_size=True)
+        t = torch.from_numpy(typ).cuda()
+        la_d = torch.from_numpy(la.view(np.int64)).cuda()
+        sz = torch.from_numpy(size.view(np.int32)).cuda()
+        _, wb = M.mori_evict_workspace(N)
+        ws = torch.empty(wb, dtype=torch.uint8, device="cuda")
+        order = torch.empty(N, dtype=torch.int32, device="cuda")
+        prefix = torch.empty(N, dtype=torch.int64, device="cuda")
+        res = torch.zeros(2, dtype=torch.int32, device="cuda")
+        blk = M.mori_blocks(N, t.data_ptr(), la_d.data_ptr(), sz.data_ptr(), 4096)
+        need = int(size.astype(np.int64).sum()) * 4096 // 4
+        s = torch.cuda.current_stream()
+        times = []
+        for _ in range(reps + 2):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            assert M.mori_evict_order(blk, 0, need, ws.data_ptr(), wb, order.data_ptr(), prefix.data_ptr(),
+                                      res.data_ptr(), s.cuda_stream) == 0
+            e1.record(s)
+            e1.synchronize()
+            times.append(e0.elapsed_time(e1) * 1e3)
+        us = sorted(times[2:])[reps // 2]
+        t0 = time.perf_counter()
+        rc, o_order, o_prefix, o_count = oracle.evict_order(typ, la, 0, need, size=size, unit_bytes=4096)
+        oracle_us = (time.perf_counter() - t0) * 1e6
+        ok = (rc == 0 and np.array_equal(order.cpu().numpy().view(np.uint32), o_order)
+              and np.array_equal(prefix.cpu().numpy().view(np.uint64), o_prefix) and int(res[0]) == o_count
+              and int(res[1]) == 0)
+        out.append({"blocks": N, "us": round(us, 1), "Mblocks_per_s": round(N / us, 1),
+                    "oracle_us_1_thread": round(oracle_us, 1), "parity_exact": bool(ok)})
+    return out
 
 
 def stored_traffic(workload: str, direction: int):
@@ -324,6 +368,10 @@ def main() -> int:
         verify = verify_sampled(inst, tp, bank, history, wins, bg, bc, valid, args, M, torch, np, run_content)
         log(f"verify: {verify}")
 
+    evict = None if args.no_evict else evict_leg(torch, np, M, (g.num_blocks, 1 << 20))
+    if evict:
+        log(f"evict order: {evict}")
+
     out = {
         "metric": "KV migration GB/s (D2H+H2D) vs host-link peak; gather/scatter HBM GB/s",
         "value": round(value, 3),
@@ -359,6 +407,7 @@ def main() -> int:
         "direction_ms_per_step": {"swap_out": round(span[0] / args.steps, 2), "swap_in": round(span[1] / args.steps, 2)},
         "cpu_baseline": cpu,
         "parity": verify,
+        "evict_order": evict,
     }
     print(json.dumps(out), flush=True)
     tp.close()

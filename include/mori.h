@@ -74,7 +74,8 @@ extern "C" {
 #define MORI_DEV_NONRES_PAGE 0x080u   /* a CPU/Waiting program's table holds a page */
 #define MORI_DEV_NOSPC 0x100u         /* not enough pages (unreachable for a consistent pool) */
 #define MORI_DEV_HOST_ADDR 0x200u     /* swap address not 16-B aligned or outside registered memory */
-/* classes: program data = 0x00F, pool state = 0x0F0, capacity = 0x100, swap = 0x200 */
+#define MORI_DEV_BAD_BLOCK 0x400u     /* eviction order: type label > 2 or last access >= 2^62 */
+/* classes: program data = 0x00F, pool state = 0x0F0, capacity = 0x100, swap = 0x200, blocks = 0x400 */
 
 /* ---- tiers, table sentinel, flags, copy modes -------------------------- */
 #define MORI_TIER_GPU 0u
@@ -232,6 +233,41 @@ int mori_query(mori_ctx* ctx, int what, uint64_t* value);
 
 /* Static description of a return code. */
 const char* mori_strerror(int code);
+
+/* ---- typed eviction order (Sec. 4.3.2) -------------------------------------- */
+/* The engine-side companion of the placement: every KV block carries the type
+ * label of its program -- busy (GPU queue), idle (CPU queue), inactive
+ * (Waiting) -- and its last access time.  A tier evicts by type first, in
+ * tier-reversed order (GPU: inactive, idle, busy; CPU: inactive, busy, idle),
+ * least recently used first within a type, so each tier keeps the programs
+ * the placement assigned to it.  Equal type and time: lowest block id first. */
+#define MORI_TYPE_BUSY 0u
+#define MORI_TYPE_IDLE 1u
+#define MORI_TYPE_INACTIVE 2u
+
+typedef struct {
+  uint32_t num_blocks;          /* N */
+  const uint8_t* type;          /* device [N] MORI_TYPE_* */
+  const uint64_t* last_access;  /* device [N] access times, larger = more recent, < 2^62 */
+  const uint32_t* size;         /* device [N] block sizes in units of unit_bytes, or NULL: one unit each */
+  uint64_t unit_bytes;
+} mori_blocks;
+
+/* Bytes of device workspace mori_evict_order needs for num_blocks blocks
+ * (about 32 bytes per block). */
+int mori_evict_workspace(uint32_t num_blocks, uint64_t* bytes);
+
+/* Eviction order of one tier (MORI_TIER_GPU or MORI_TIER_CPU), enqueued on
+ * `stream`: order[j] (device [N]) = block evicted j-th; prefix[j] (device [N],
+ * may be NULL) = bytes freed by the first j+1 evictions; result (device [2]) =
+ * {fewest evictions that free at least need_bytes (N if all of them free
+ * less, 0 when need_bytes is 0), MORI_DEV_* error bits}.  workspace: device
+ * memory of at least mori_evict_workspace bytes, 256-B aligned, owned by the
+ * caller and used only while the call's work runs.  Nothing is allocated.
+ * EINVAL: null pointers, misaligned or short workspace, bad tier. */
+int mori_evict_order(const mori_blocks* blocks, uint32_t tier, uint64_t need_bytes, void* workspace,
+                     uint64_t workspace_bytes, uint32_t* order, uint64_t* prefix, uint32_t* result,
+                     void* stream);
 
 /* ---- kernel timing ------------------------------------------------------ */
 /* With profiling on, every gather/scatter kernel launch of the swaps is

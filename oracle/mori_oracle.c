@@ -340,3 +340,56 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
   free(new_tbl);
   return rc;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Typed eviction order (Sec. 4.3.2).                                         */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+  uint32_t rank_of_type; /* position of the block's type in the tier's eviction order */
+  uint64_t time;
+  uint32_t id;
+} orc_victim;
+
+static int orc_victim_cmp(const void* a, const void* b) {
+  const orc_victim* x = (const orc_victim*)a;
+  const orc_victim* y = (const orc_victim*)b;
+  if (x->rank_of_type != y->rank_of_type) return x->rank_of_type < y->rank_of_type ? -1 : 1;
+  if (x->time != y->time) return x->time < y->time ? -1 : 1; /* least recently used first */
+  if (x->id != y->id) return x->id < y->id ? -1 : 1;
+  return 0;
+}
+
+int orc_evict_order(uint32_t N, const uint8_t* type, const uint64_t* last_access, const uint32_t* size,
+                    uint64_t unit_bytes, uint32_t tier, uint64_t need_bytes, uint32_t* order, uint64_t* prefix,
+                    uint32_t* count) {
+  /* tier-reversed type order: GPU evicts inactive, idle, busy; CPU evicts inactive, busy, idle */
+  static const uint32_t gpu_rank[3] = {2, 1, 0}; /* indexed by type: busy, idle, inactive */
+  static const uint32_t cpu_rank[3] = {1, 2, 0};
+  if (tier != ORC_GPU && tier != ORC_CPU) return ORC_E_INPUT;
+  const uint32_t* rank_of = tier == ORC_GPU ? gpu_rank : cpu_rank;
+  for (uint32_t b = 0; b < N; ++b)
+    if (type[b] > ORC_TYPE_INACTIVE) return ORC_E_INPUT;
+  orc_victim* v = (orc_victim*)malloc(sizeof(orc_victim) * (N ? N : 1));
+  for (uint32_t b = 0; b < N; ++b) {
+    v[b].rank_of_type = rank_of[type[b]];
+    v[b].time = last_access[b];
+    v[b].id = b;
+  }
+  qsort(v, N, sizeof(orc_victim), orc_victim_cmp);
+  uint64_t freed = 0;
+  uint32_t m = N;
+  int found = 0;
+  for (uint32_t j = 0; j < N; ++j) {
+    order[j] = v[j].id;
+    freed += (uint64_t)(size ? size[v[j].id] : 1u) * unit_bytes;
+    if (prefix) prefix[j] = freed;
+    if (!found && freed >= need_bytes) {
+      m = j + 1;
+      found = 1;
+    }
+  }
+  if (need_bytes == 0) m = 0;
+  *count = m;
+  free(v);
+  return ORC_OK;
+}

@@ -102,6 +102,28 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
                   uint8_t* const* host_bufs, uint32_t* order, uint32_t* rank, uint8_t* tier_old_out,
                   uint8_t* category, uint64_t* prefix, orc_summary* summary);
 
+/* ------------------------------------------------------------------------ */
+/* Typed eviction order (Sec. 4.3.2, typed offloading on the engine).        */
+/* Every KV block carries its program's type label -- busy (GPU queue), idle */
+/* (CPU queue) or inactive (Waiting) -- and its last access time.  Eviction */
+/* is least-recently-used within a type, with the type as the higher key,    */
+/* in tier-reversed order: the GPU tier evicts inactive, then idle, then     */
+/* busy blocks; the CPU tier evicts inactive, then busy, then idle blocks.   */
+/* ------------------------------------------------------------------------ */
+#define ORC_TYPE_BUSY 0u
+#define ORC_TYPE_IDLE 1u
+#define ORC_TYPE_INACTIVE 2u
+
+/* order[j] = block evicted j-th from `tier` (ORC_GPU or ORC_CPU).  prefix[j] =
+ * bytes freed by the first j+1 evictions (size[b] * unit_bytes each; size may
+ * be NULL for one unit per block).  *count = fewest evictions that free at
+ * least need_bytes (all N when even all of them free less).  Reading: equal
+ * type and time go lowest block id first.  Returns ORC_E_INPUT for a type
+ * label above 2 or a tier other than GPU/CPU. */
+int orc_evict_order(uint32_t N, const uint8_t* type, const uint64_t* last_access, const uint32_t* size,
+                    uint64_t unit_bytes, uint32_t tier, uint64_t need_bytes, uint32_t* order, uint64_t* prefix,
+                    uint32_t* count);
+
 #ifdef __cplusplus
 }
 #endif

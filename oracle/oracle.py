@@ -22,6 +22,7 @@ SRC = os.path.join(HERE, "mori_oracle.c")
 LIB = os.path.join(HERE, "liboracle.so")
 
 GPU, CPU, WAIT = 0, 1, 2
+TYPE_BUSY, TYPE_IDLE, TYPE_INACTIVE = 0, 1, 2
 NONE = 0xFFFFFFFF
 F_STATUS_KEY, F_SKIP_FIT, F_IDLENESS_GIVEN = 1, 2, 4
 OK, E_INPUT, E_POOL, E_NOSPC = 0, 1, 2, 3
@@ -72,6 +73,7 @@ def lib():
         _lib.orc_boundary.restype = None
         _lib.orc_rebalance.argtypes = [P, P, C.c_uint32, C.c_uint32, P, P, P, P, C.c_uint32, P, P, P,
                                        C.c_uint64, C.c_uint64, C.c_uint32, P, P, P, P, P, P, P]
+        _lib.orc_evict_order.argtypes = [C.c_uint32, P, P, P, C.c_uint64, C.c_uint32, C.c_uint64, P, P, P]
     return _lib
 
 
@@ -175,3 +177,17 @@ def rebalance(geom, *, window=None, iota=None, status=None, tbl_off, tbl, tier, 
                              _ptr(order_), _ptr(rank), _ptr(tier_old), _ptr(cat), _ptr(prefix), C.byref(s))
     summary = {name: getattr(s, name) for name, _ in _Summary._fields_} if rc == OK else {}
     return Result(rc, order_, rank, tier_old, cat, prefix, summary)
+
+
+def evict_order(type_, last_access, tier, need_bytes, size=None, unit_bytes=1):
+    """Typed eviction order of one tier (Sec. 4.3.2) -> (rc, order, prefix, count)."""
+    t = _need(type_, np.uint8)
+    la = _need(last_access, np.uint64, t.size)
+    sz = None if size is None else _need(size, np.uint32, t.size)
+    N = t.size
+    order_ = np.zeros(N, np.uint32)
+    prefix = np.zeros(N, np.uint64)
+    cnt = C.c_uint32(0)
+    rc = lib().orc_evict_order(N, _ptr(t), _ptr(la), _ptr(sz), int(unit_bytes), int(tier), int(need_bytes),
+                               _ptr(order_), _ptr(prefix), C.byref(cnt))
+    return rc, order_, prefix, cnt.value

@@ -683,6 +683,29 @@ extern "C" int mori_query(mori_ctx* ctx, int what, uint64_t* value) {
   }
 }
 
+extern "C" int mori_evict_workspace(uint32_t num_blocks, uint64_t* bytes) {
+  if (!bytes) return MORI_EINVAL;
+  *bytes = evict_workspace_bytes(num_blocks);
+  return MORI_OK;
+}
+
+extern "C" int mori_evict_order(const mori_blocks* b, uint32_t tier, uint64_t need_bytes, void* workspace,
+                                uint64_t workspace_bytes, uint32_t* order, uint64_t* prefix, uint32_t* result,
+                                void* stream) {
+  if (!b || !workspace || !result) return MORI_EINVAL;
+  if (tier != MORI_TIER_GPU && tier != MORI_TIER_CPU) return MORI_EINVAL;
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u) return MORI_EINVAL;
+  if (workspace_bytes < evict_workspace_bytes(b->num_blocks)) return MORI_EINVAL;
+  if (b->num_blocks && (!b->type || !b->last_access || !order)) return MORI_EINVAL;
+  const hipError_t e = launch_evict(b->num_blocks, b->type, b->last_access, b->size, b->unit_bytes, tier,
+                                    need_bytes, workspace, order, prefix, result, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return MORI_EHIP;
+  }
+  return MORI_OK;
+}
+
 extern "C" int mori_profile(mori_ctx* ctx, int enable) {
   if (!ctx) return MORI_EINVAL;
   if (enable && ctx->prof_ev[0].empty()) {

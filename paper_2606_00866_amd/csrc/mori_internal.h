@@ -103,5 +103,9 @@ hipError_t launch_pages(const PlanArgs& a, hipStream_t s);
 hipError_t launch_translate(const TranslateArgs& a, hipStream_t s);
 hipError_t launch_swap_out(const SwapArgs& a, uint32_t grid, hipStream_t s);
 hipError_t launch_swap_in(const SwapArgs& a, uint32_t grid, hipStream_t s);
+uint64_t evict_workspace_bytes(uint32_t N);
+hipError_t launch_evict(uint32_t N, const uint8_t* type, const uint64_t* last_access, const uint32_t* size,
+                        uint64_t unit_bytes, uint32_t tier, uint64_t need, void* workspace, uint32_t* order,
+                        uint64_t* prefix, uint32_t* result, hipStream_t s);
 
 }  // namespace mori

@@ -16,7 +16,8 @@ LIB_PATH = os.path.join(HERE, "libmori.so")
 MORI_OK, MORI_EINVAL, MORI_ENOSPC, MORI_ESTATE, MORI_EHIP, MORI_EDEVICE = 0, -1, -2, -3, -4, -5
 MORI_DEV_BAD_WINDOW, MORI_DEV_BAD_IDLENESS, MORI_DEV_BAD_TIER, MORI_DEV_BAD_TBL_OFF = 0x1, 0x2, 0x4, 0x8
 MORI_DEV_PAGE_RANGE, MORI_DEV_PAGE_DUP, MORI_DEV_PAGE_LEAK, MORI_DEV_NONRES_PAGE = 0x10, 0x20, 0x40, 0x80
-MORI_DEV_NOSPC, MORI_DEV_HOST_ADDR = 0x100, 0x200
+MORI_DEV_NOSPC, MORI_DEV_HOST_ADDR, MORI_DEV_BAD_BLOCK = 0x100, 0x200, 0x400
+MORI_TYPE_BUSY, MORI_TYPE_IDLE, MORI_TYPE_INACTIVE = 0, 1, 2
 MORI_TIER_GPU, MORI_TIER_CPU, MORI_TIER_WAIT = 0, 1, 2
 MORI_NO_PAGE = 0xFFFFFFFF
 MORI_F_STATUS_KEY, MORI_F_SKIP_FIT, MORI_F_IDLENESS_GIVEN = 1, 2, 4
@@ -29,7 +30,7 @@ MORI_Q_PLAN_EVENT, MORI_Q_OUT_EVENT, MORI_Q_IN_EVENT = 4, 5, 6
 
 EXPORTS = ("mori_create", "mori_destroy", "mori_register", "mori_host_alloc", "mori_host_free",
            "mori_rank_partition", "mori_plan_wait", "mori_kv_swap_out", "mori_kv_swap_in", "mori_query",
-           "mori_strerror", "mori_profile", "mori_profile_read")
+           "mori_strerror", "mori_profile", "mori_profile_read", "mori_evict_workspace", "mori_evict_order")
 
 
 class mori_pool(C.Structure):
@@ -45,6 +46,11 @@ class mori_programs(C.Structure):
 
 class mori_budget(C.Structure):
     _fields_ = [("gpu_bytes", C.c_uint64), ("cpu_bytes", C.c_uint64), ("flags", C.c_uint32)]
+
+
+class mori_blocks(C.Structure):
+    _fields_ = [("num_blocks", C.c_uint32), ("type", C.c_void_p), ("last_access", C.c_void_p),
+                ("size", C.c_void_p), ("unit_bytes", C.c_uint64)]
 
 
 class mori_plan(C.Structure):
@@ -82,6 +88,8 @@ def lib():
         L.mori_strerror.argtypes = [I]
         L.mori_profile.argtypes = [V, I]
         L.mori_profile_read.argtypes = [V, I, C.POINTER(U64), C.POINTER(U64), C.POINTER(C.c_double)]
+        L.mori_evict_workspace.argtypes = [U32, C.POINTER(U64)]
+        L.mori_evict_order.argtypes = [C.POINTER(mori_blocks), U32, U64, V, U64, V, V, V, V]
         L.mori_strerror.restype = C.c_char_p
         for name in EXPORTS:
             if name != "mori_strerror":
@@ -152,3 +160,16 @@ def mori_profile_read(ctx, direction: int):
     n, by, ms = C.c_uint64(), C.c_uint64(), C.c_double()
     rc = lib().mori_profile_read(ctx, direction, C.byref(n), C.byref(by), C.byref(ms))
     return rc, n.value, by.value, ms.value
+
+
+def mori_evict_workspace(num_blocks: int):
+    b = C.c_uint64()
+    rc = lib().mori_evict_workspace(num_blocks, C.byref(b))
+    return rc, b.value
+
+
+def mori_evict_order(blocks: mori_blocks, tier: int, need_bytes: int, workspace: int, workspace_bytes: int,
+                     order: int, prefix: int, result: int, stream: int = 0) -> int:
+    """order / prefix / result / workspace: device addresses (prefix may be 0)."""
+    return lib().mori_evict_order(C.byref(blocks), tier, need_bytes, workspace, workspace_bytes, order,
+                                  prefix or None, result, stream)

@@ -1,0 +1,102 @@
+"""GPU parity of the typed eviction order (Sec. 4.3.2): libmori's device radix
+sort and reclaim prefix against the oracle, element by element."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import log
+from oracle import oracle
+from paper_2606_00866_amd import mori as M
+from workload import eviction_blocks
+
+pytestmark = pytest.mark.gpu
+
+
+def run_gpu(typ, la, size, unit, tier, need):
+    N = typ.size
+    dev = "cuda"
+    t = torch.from_numpy(np.ascontiguousarray(typ, np.uint8)).to(dev)
+    l = torch.from_numpy(np.ascontiguousarray(la, np.uint64).view(np.int64)).to(dev)
+    sz = None if size is None else torch.from_numpy(np.ascontiguousarray(size, np.uint32).view(np.int32)).to(dev)
+    rc, wbytes = M.mori_evict_workspace(N)
+    assert rc == 0
+    ws = torch.empty(max(wbytes, 256), dtype=torch.uint8, device=dev)
+    order = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
+    prefix = torch.empty(max(N, 1), dtype=torch.int64, device=dev)
+    result = torch.zeros(2, dtype=torch.int32, device=dev)
+    blk = M.mori_blocks(N, t.data_ptr() if N else None, l.data_ptr() if N else None,
+                        sz.data_ptr() if sz is not None else None, unit)
+    rc = M.mori_evict_order(blk, tier, need, ws.data_ptr(), ws.numel(), order.data_ptr(), prefix.data_ptr(),
+                            result.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    assert rc == 0
+    torch.cuda.synchronize()
+    return (order.cpu().numpy().view(np.uint32)[:N], prefix.cpu().numpy().view(np.uint64)[:N],
+            result.cpu().numpy().view(np.uint32))
+
+
+def check(typ, la, size, unit, tier, need):
+    rc, o_order, o_prefix, o_count = oracle.evict_order(typ, la, tier, need, size=size, unit_bytes=unit)
+    assert rc == oracle.OK
+    g_order, g_prefix, res = run_gpu(typ, la, size, unit, tier, need)
+    assert res[1] == 0
+    assert np.array_equal(g_order, o_order), "order"
+    assert np.array_equal(g_prefix, o_prefix), "prefix"
+    assert res[0] == o_count, ("count", res[0], o_count)
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_small(seed):
+    rng = np.random.default_rng(seed)
+    N = int(rng.choice([0, 1, 2, 17, 255, 256, 4095, 4096, 4097, 9000, 20000]))
+    typ, la, size = eviction_blocks(rng, N, programs=int(rng.integers(1, 64)), tie_frac=float(rng.random()),
+                                    horizon=int(rng.choice([8, 1 << 20, 1 << 44])), var_size=bool(seed % 2))
+    tier = seed % 2
+    total = int(N if size is None else size.astype(np.int64).sum())
+    need = int(rng.integers(0, 2 * total + 2)) * 3
+    log(f"evict seed={seed} N={N} tier={tier} need={need}")
+    check(typ, la, size, 3, tier, need)
+
+
+def test_degenerate_keys():
+    """All keys equal (every radix pass is skipped) and a single varying digit."""
+    N = 10000
+    check(np.zeros(N, np.uint8), np.full(N, 7, np.uint64), None, 1, 0, 5000)
+    la = np.zeros(N, np.uint64)
+    la[::3] = 255
+    check(np.ones(N, np.uint8), la, None, 2, 1, 1)
+    check(np.full(N, 2, np.uint8), np.full(N, (1 << 62) - 1, np.uint64), None, 1, 0, N + 5)
+
+
+@pytest.mark.parametrize("N", [69938, 1 << 20])
+def test_large(N):
+    rng = np.random.default_rng(N)
+    typ, la, size = eviction_blocks(rng, N, programs=1024, tie_frac=0.5)
+    log(f"evict large N={N}")
+    for tier in (0, 1):
+        check(typ, la, size, 2 << 20, tier, (N // 3) * (2 << 20))
+
+
+def test_bad_blocks_reported():
+    typ = np.zeros(100, np.uint8)
+    typ[40] = 3
+    _, _, res = run_gpu(typ, np.zeros(100, np.uint64), None, 1, 0, 10)
+    assert res[1] & M.MORI_DEV_BAD_BLOCK and res[0] == 0
+    la = np.zeros(100, np.uint64)
+    la[7] = 1 << 62
+    _, _, res = run_gpu(np.zeros(100, np.uint8), la, None, 1, 1, 10)
+    assert res[1] & M.MORI_DEV_BAD_BLOCK
+
+
+def test_host_side_argument_errors():
+    rc, w = M.mori_evict_workspace(1000)
+    assert rc == 0 and w >= 32 * 1000
+    ws = torch.empty(w, dtype=torch.uint8, device="cuda")
+    res = torch.zeros(2, dtype=torch.int32, device="cuda")
+    t = torch.zeros(1000, dtype=torch.uint8, device="cuda")
+    l = torch.zeros(1000, dtype=torch.int64, device="cuda")
+    o = torch.zeros(1000, dtype=torch.int32, device="cuda")
+    blk = M.mori_blocks(1000, t.data_ptr(), l.data_ptr(), None, 1)
+    assert M.mori_evict_order(blk, 2, 0, ws.data_ptr(), w, o.data_ptr(), 0, res.data_ptr()) == M.MORI_EINVAL
+    assert M.mori_evict_order(blk, 0, 0, ws.data_ptr(), w - 8, o.data_ptr(), 0, res.data_ptr()) == M.MORI_EINVAL
+    assert M.mori_evict_order(blk, 0, 0, ws.data_ptr() + 8, w, o.data_ptr(), 0, res.data_ptr()) == M.MORI_EINVAL
+    assert M.mori_evict_order(blk, 0, 0, ws.data_ptr(), w, 0, 0, res.data_ptr()) == M.MORI_EINVAL

@@ -370,3 +370,30 @@ def program_content_torch(inst: Instance, bank_dev, p: int, out=None):
         out.copy_(vals)
         return out
     return vals
+
+
+def eviction_blocks(rng, N: int, programs: int = 256, type_p=(0.5, 0.3, 0.2), tie_frac: float = 0.5,
+                    horizon: int = 1 << 40, var_size: bool = False):
+    """KV blocks for the typed eviction order: N blocks dealt to programs in
+    contiguous runs; each program draws a type label (busy / idle / inactive
+    with probabilities type_p) and a last-activity time in [0, horizon) us.
+    A fraction tie_frac of programs stamp every block with that time (their
+    whole prefix is touched by each request, so ties are common); the others'
+    blocks are older by a random step per block.  Sizes: one unit per block,
+    or 1..16 units (radix-tree nodes of varying token counts)."""
+    programs = max(1, min(programs, max(N, 1)))
+    cuts = np.sort(rng.choice(np.arange(1, max(N, 2)), size=min(programs - 1, max(N - 1, 0)), replace=False)) \
+        if N > 1 else np.zeros(0, np.int64)
+    owner = np.zeros(N, np.int64)
+    if N:
+        owner[cuts] = 1
+        owner = np.cumsum(owner)
+    P = int(owner[-1]) + 1 if N else 0
+    ptype = rng.choice(3, size=P, p=list(type_p)).astype(np.uint8)
+    ptime = rng.integers(0, horizon, size=P, dtype=np.int64)
+    tied = rng.random(P) < tie_frac
+    steps = rng.integers(1, 1 << 20, size=N, dtype=np.int64)
+    t = ptime[owner] - np.where(tied[owner], 0, steps)
+    t = np.clip(t, 0, None).astype(np.uint64)
+    size = rng.integers(1, 17, size=N).astype(np.uint32) if var_size else None
+    return ptype[owner], t, size
