@@ -152,6 +152,171 @@ static uint8_t orc_category(uint8_t from, uint8_t to) {
 }
 
 /* ------------------------------------------------------------------------ */
+/* Incremental sticky placement (Sec. 4.3 "sticky placement"; Sec. 4.3.1     */
+/* demotion from GPU and promotion to GPU).  Written as the loops the paper  */
+/* describes: pick the next victim while a tier is over budget, then promote */
+/* while the next candidate fits.                                            */
+/* Readings: programs of equal status and idleness are demoted highest id    */
+/* first and promoted lowest id first (the reverse of each other, as in the  */
+/* ranking); the CPU tier is brought within its budget before the GPU's      */
+/* victims are placed; each victim goes to the CPU tier if it fits in what   */
+/* is left there (the paper's per-program rule); promotion stops at the      */
+/* first candidate that does not fit so that no lower-priority program       */
+/* overtakes it (ORC_F_SKIP_FIT skips it instead); a program moved by this   */
+/* step is not promoted again in it; a new arrival found outside Waiting     */
+/* counts as Reasoning; Waiting programs are never placed on the CPU tier    */
+/* (their KV is rebuilt by prefill on the GPU).                              */
+/* ------------------------------------------------------------------------ */
+static int orc_is_acting(const uint8_t* status, uint32_t p) { return status[p] == ORC_ST_ACTING; }
+
+/* nonzero when program x is demoted before program y */
+static int orc_demote_before(const float* iota, const uint8_t* status, uint32_t x, uint32_t y) {
+  int ax = orc_is_acting(status, x), ay = orc_is_acting(status, y);
+  if (ax != ay) return ax; /* Acting (KV idle on the GPU) before Reasoning */
+  if (iota[x] != iota[y]) return iota[x] > iota[y];
+  return x > y;
+}
+
+/* promotion level of a candidate: 0 CPU tier, 1 returning Waiting, 2 new arrival */
+static uint32_t orc_promote_level(const uint8_t* status, const uint8_t* tier_old, uint32_t p) {
+  if (tier_old[p] == ORC_CPU) return 0;
+  return status[p] == ORC_ST_NEW ? 2 : 1;
+}
+
+/* comparison context for qsort (single-threaded oracle) */
+static const float* orc_sort_iota;
+static const uint8_t* orc_sort_status;
+static const uint8_t* orc_sort_tier;
+static const uint32_t* orc_sort_nblk;
+
+static int orc_promote_cmp(const void* a, const void* b) {
+  uint32_t x = *(const uint32_t*)a, y = *(const uint32_t*)b;
+  uint32_t lx = orc_promote_level(orc_sort_status, orc_sort_tier, x);
+  uint32_t ly = orc_promote_level(orc_sort_status, orc_sort_tier, y);
+  if (lx != ly) return lx < ly ? -1 : 1;
+  if (lx == 2 && orc_sort_nblk[x] != orc_sort_nblk[y]) return orc_sort_nblk[x] < orc_sort_nblk[y] ? -1 : 1;
+  if (orc_sort_iota[x] != orc_sort_iota[y]) return orc_sort_iota[x] < orc_sort_iota[y] ? -1 : 1;
+  return x < y ? -1 : (x > y);
+}
+
+/* listing group of a program: 0 GPU, 1 CPU, 2 Waiting Reasoning, 3 Waiting new, 4 Waiting Acting */
+static uint32_t orc_list_group(uint32_t p) {
+  if (orc_sort_tier[p] == ORC_GPU) return 0;
+  if (orc_sort_tier[p] == ORC_CPU) return 1;
+  if (orc_sort_status[p] == ORC_ST_ACTING) return 4;
+  return orc_sort_status[p] == ORC_ST_NEW ? 3 : 2;
+}
+
+static int orc_list_cmp(const void* a, const void* b) {
+  uint32_t x = *(const uint32_t*)a, y = *(const uint32_t*)b;
+  uint32_t gx = orc_list_group(x), gy = orc_list_group(y);
+  if (gx != gy) return gx < gy ? -1 : 1;
+  if (gx <= 1) { /* the reverse of the demotion order */
+    if (x == y) return 0;
+    return orc_demote_before(orc_sort_iota, orc_sort_status, x, y) ? 1 : -1;
+  }
+  if (gx == 3 && orc_sort_nblk[x] != orc_sort_nblk[y]) return orc_sort_nblk[x] < orc_sort_nblk[y] ? -1 : 1;
+  if (orc_sort_iota[x] != orc_sort_iota[y]) return orc_sort_iota[x] < orc_sort_iota[y] ? -1 : 1;
+  return x < y ? -1 : (x > y);
+}
+
+int orc_incremental(uint32_t P, const float* iota_in, const uint8_t* status, const uint8_t* tier_old,
+                    const uint32_t* nblk, uint64_t block_bytes, uint64_t gpu_budget, uint64_t cpu_budget,
+                    uint32_t flags, uint32_t* order, uint32_t* rank, uint64_t* prefix, uint8_t* tier_new,
+                    uint32_t* m_gpu, uint32_t* m_cpu) {
+  const size_t np = P ? P : 1;
+  float* iota = (float*)malloc(sizeof(float) * np);
+  for (uint32_t p = 0; p < P; ++p) {
+    float v = iota_in[p];
+    if (!(v >= 0.0f && v <= 1.0f) || status[p] > ORC_ST_NEW ||
+        (tier_old[p] == ORC_WAIT && status[p] == ORC_ST_NEW && nblk[p] >= 0x80000000u)) {
+      free(iota);
+      return ORC_E_INPUT;
+    }
+    iota[p] = (v == 0.0f) ? 0.0f : v;
+  }
+  uint8_t* moved = (uint8_t*)calloc(np, 1);
+  uint32_t* cand = (uint32_t*)malloc(sizeof(uint32_t) * np);
+  uint64_t used_gpu = 0, used_cpu = 0;
+  for (uint32_t p = 0; p < P; ++p) {
+    tier_new[p] = tier_old[p];
+    uint64_t bytes = (uint64_t)nblk[p] * block_bytes;
+    if (tier_old[p] == ORC_GPU) used_gpu += bytes;
+    if (tier_old[p] == ORC_CPU) used_cpu += bytes;
+  }
+
+  /* 1. CPU admission control */
+  while (used_cpu > cpu_budget) {
+    uint32_t v = P;
+    for (uint32_t p = 0; p < P; ++p)
+      if (tier_new[p] == ORC_CPU && tier_old[p] == ORC_CPU && !moved[p] &&
+          (v == P || orc_demote_before(iota, status, p, v)))
+        v = p;
+    tier_new[v] = ORC_WAIT;
+    moved[v] = 1;
+    used_cpu -= (uint64_t)nblk[v] * block_bytes;
+  }
+
+  /* 2. demotion from GPU */
+  while (used_gpu > gpu_budget) {
+    uint32_t v = P;
+    for (uint32_t p = 0; p < P; ++p)
+      if (tier_new[p] == ORC_GPU && (v == P || orc_demote_before(iota, status, p, v))) v = p;
+    uint64_t bytes = (uint64_t)nblk[v] * block_bytes;
+    used_gpu -= bytes;
+    moved[v] = 1;
+    if (bytes <= cpu_budget - used_cpu) {
+      tier_new[v] = ORC_CPU;
+      used_cpu += bytes;
+    } else {
+      tier_new[v] = ORC_WAIT;
+    }
+  }
+
+  /* 3. promotion to GPU */
+  uint32_t nc = 0;
+  for (uint32_t p = 0; p < P; ++p)
+    if (!moved[p] && tier_old[p] != ORC_GPU && status[p] != ORC_ST_ACTING) cand[nc++] = p;
+  orc_sort_iota = iota;
+  orc_sort_status = status;
+  orc_sort_tier = tier_old;
+  orc_sort_nblk = nblk;
+  qsort(cand, nc, sizeof(uint32_t), orc_promote_cmp);
+  uint64_t room = gpu_budget - used_gpu;
+  for (uint32_t j = 0; j < nc; ++j) {
+    uint32_t p = cand[j];
+    uint64_t bytes = (uint64_t)nblk[p] * block_bytes;
+    if (bytes <= room) {
+      room -= bytes;
+      tier_new[p] = ORC_GPU;
+    } else if (!(flags & ORC_F_SKIP_FIT)) {
+      break;
+    }
+  }
+
+  /* the listing order and the byte prefix along it */
+  for (uint32_t p = 0; p < P; ++p) order[p] = p;
+  qsort(order, P, sizeof(uint32_t), orc_list_cmp);
+  uint64_t running = 0;
+  uint32_t ng = 0, nk = 0;
+  for (uint32_t r = 0; r < P; ++r) {
+    running += (uint64_t)nblk[order[r]] * block_bytes;
+    prefix[r] = running;
+    if (rank) rank[order[r]] = r;
+  }
+  for (uint32_t p = 0; p < P; ++p) {
+    ng += tier_new[p] == ORC_GPU;
+    nk += tier_new[p] == ORC_CPU;
+  }
+  *m_gpu = ng;
+  *m_cpu = nk;
+  free(iota);
+  free(moved);
+  free(cand);
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
 /* One rebalance.                                                            */
 /* ------------------------------------------------------------------------ */
 int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32_t k,
@@ -198,14 +363,21 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
       rc = orc_idleness(P, k, window, iota);
     }
   }
-  if (rc == ORC_OK) rc = orc_keys(P, iota, status, flags, key);
   uint32_t m_gpu = 0, m_cpu = 0;
-  if (rc == ORC_OK) {
-    orc_order(P, key, order, rank);
-    orc_boundary(P, order, nblk, block_bytes, gpu_budget, cpu_budget, flags, prefix, tier_new,
-                 &m_gpu, &m_cpu);
-    for (uint32_t p = 0; p < P; ++p) cat[p] = orc_category(tier[p], tier_new[p]);
+  if (rc == ORC_OK && (flags & ORC_F_INCREMENTAL)) {
+    if (status == NULL && P) rc = ORC_E_INPUT;
+    else rc = orc_incremental(P, iota, status, tier, nblk, block_bytes, gpu_budget, cpu_budget, flags, order,
+                              rank, prefix, tier_new, &m_gpu, &m_cpu);
+  } else if (rc == ORC_OK) {
+    rc = orc_keys(P, iota, status, flags, key);
+    if (rc == ORC_OK) {
+      orc_order(P, key, order, rank);
+      orc_boundary(P, order, nblk, block_bytes, gpu_budget, cpu_budget, flags, prefix, tier_new,
+                   &m_gpu, &m_cpu);
+    }
   }
+  if (rc == ORC_OK)
+    for (uint32_t p = 0; p < P; ++p) cat[p] = orc_category(tier[p], tier_new[p]);
 
   /* -- pool consistency: every page is either free or owned by exactly one
         GPU-resident program; non-resident programs hold no page -- */

@@ -44,6 +44,14 @@ extern "C" {
 #define ORC_F_STATUS_KEY 1u     /* Acting programs rank after Reasoning ones (Sec. 4.3.1, demotion) */
 #define ORC_F_SKIP_FIT 2u       /* greedy fit instead of a strict prefix boundary */
 #define ORC_F_IDLENESS_GIVEN 4u /* idleness supplied directly instead of windows */
+#define ORC_F_INCREMENTAL 8u    /* incremental sticky policy (Sec. 4.3.1) instead of the boundary */
+
+/* program status (Sec. 4.1): Reasoning = running or waiting for inference,
+   Acting = inside a tool call, New = arrived and not yet run (waits for its
+   first inference, no KV anywhere) */
+#define ORC_ST_REASONING 0u
+#define ORC_ST_ACTING 1u
+#define ORC_ST_NEW 2u
 
 /* result classes */
 #define ORC_OK 0
@@ -87,6 +95,33 @@ void orc_boundary(uint32_t P, const uint32_t* order, const uint32_t* nblk, uint6
                   uint64_t gpu_budget, uint64_t cpu_budget, uint32_t flags, uint64_t* prefix,
                   uint8_t* tier_new, uint32_t* m_gpu, uint32_t* m_cpu);
 
+/* Incremental sticky placement (Sec. 4.3 and Sec. 4.3.1), the alternative to
+ * the boundary: tiers change only to repair a capacity violation or to fill
+ * free GPU capacity.
+ *   1. CPU admission control: while the CPU tier holds more than its budget,
+ *      its programs go to Waiting in demotion order.
+ *   2. Demotion from GPU: while the GPU tier holds more than its budget, the
+ *      next program in demotion order (Acting before Reasoning, then highest
+ *      idleness) leaves the GPU; it goes to the CPU tier if it fits in what
+ *      the CPU budget has left, otherwise to Waiting.  A Reasoning victim is
+ *      demoted lazily (after its current inference step) by the caller.
+ *   3. Promotion to GPU into the room left: CPU-tier programs waiting for
+ *      inference, then returning Waiting programs waiting for inference, then
+ *      new arrivals smallest context first; lowest idleness first within a
+ *      level.  Programs moved in steps 1-2 are not candidates.  The walk stops
+ *      at the first candidate that does not fit (ORC_F_SKIP_FIT: skips it).
+ * order[] lists all programs by old tier and the priorities above (GPU and CPU
+ * programs: Reasoning before Acting, then idleness; Waiting programs: returning
+ * Reasoning ones by idleness, new arrivals by context then idleness, Acting
+ * ones by idleness; ties lowest id first), so demotion runs from its end of a
+ * tier group and promotion from the start; prefix[] accumulates bytes along it.
+ * Rejects (ORC_E_INPUT) a status above 2, idleness outside [0, 1] and a new
+ * arrival with 2^31 or more blocks. */
+int orc_incremental(uint32_t P, const float* iota, const uint8_t* status, const uint8_t* tier_old,
+                    const uint32_t* nblk, uint64_t block_bytes, uint64_t gpu_budget, uint64_t cpu_budget,
+                    uint32_t flags, uint32_t* order, uint32_t* rank, uint64_t* prefix, uint8_t* tier_new,
+                    uint32_t* m_gpu, uint32_t* m_cpu);
+
 /* One whole rebalance: Eq. 1 -> ranking -> boundary -> sticky diff -> page
  * allocation -> table rewrite -> byte movement.  All state arrays are updated
  * in place only when the result is ORC_OK; on an error nothing is modified.
@@ -94,7 +129,9 @@ void orc_boundary(uint32_t P, const uint32_t* order, const uint32_t* nblk, uint6
  * pool_bytes [layers*planes][num_blocks][block_tokens*row_bytes] and host_bufs
  * [P] (one contiguous [layers*planes][nblk_p][block_tokens*row_bytes] buffer per
  * program) may both be NULL to compute the placement only.
- * Optional outputs (may be NULL): order, rank, tier_old_out, category, prefix, summary. */
+ * Optional outputs (may be NULL): order, rank, tier_old_out, category, prefix, summary.
+ * With ORC_F_INCREMENTAL the placement comes from orc_incremental (status
+ * required) instead of the ranking and boundary. */
 int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32_t k,
                   const float* window, const float* iota_given, const uint8_t* status,
                   const uint32_t* tbl_off, uint32_t tbl_len, uint32_t* tbl, uint8_t* tier,

@@ -24,7 +24,8 @@ LIB = os.path.join(HERE, "liboracle.so")
 GPU, CPU, WAIT = 0, 1, 2
 TYPE_BUSY, TYPE_IDLE, TYPE_INACTIVE = 0, 1, 2
 NONE = 0xFFFFFFFF
-F_STATUS_KEY, F_SKIP_FIT, F_IDLENESS_GIVEN = 1, 2, 4
+F_STATUS_KEY, F_SKIP_FIT, F_IDLENESS_GIVEN, F_INCREMENTAL = 1, 2, 4, 8
+ST_REASONING, ST_ACTING, ST_NEW = 0, 1, 2
 OK, E_INPUT, E_POOL, E_NOSPC = 0, 1, 2, 3
 KEPT, OUT, IN, DROP_GPU, DROP_CPU, ADMIT_GPU, ADMIT_CPU = range(7)
 
@@ -73,6 +74,8 @@ def lib():
         _lib.orc_boundary.restype = None
         _lib.orc_rebalance.argtypes = [P, P, C.c_uint32, C.c_uint32, P, P, P, P, C.c_uint32, P, P, P,
                                        C.c_uint64, C.c_uint64, C.c_uint32, P, P, P, P, P, P, P]
+        _lib.orc_incremental.argtypes = [C.c_uint32, P, P, P, P, C.c_uint64, C.c_uint64, C.c_uint64, C.c_uint32,
+                                         P, P, P, P, P, P]
         _lib.orc_evict_order.argtypes = [C.c_uint32, P, P, P, C.c_uint64, C.c_uint32, C.c_uint64, P, P, P]
     return _lib
 
@@ -123,6 +126,23 @@ def boundary(order_, nblk, block_bytes, gpu_budget, cpu_budget, flags=0):
     lib().orc_boundary(P, _ptr(o), _ptr(nb), block_bytes, gpu_budget, cpu_budget, flags, _ptr(prefix),
                        _ptr(tier_new), C.byref(mg), C.byref(mc))
     return prefix, tier_new, mg.value, mc.value
+
+
+def incremental(iota, status, tier_old, nblk, block_bytes, gpu_budget, cpu_budget, flags=0):
+    """Incremental sticky placement (Sec. 4.3.1) -> (rc, order, prefix, tier_new, m_gpu, m_cpu)."""
+    it = _need(iota, np.float32)
+    P = it.size
+    st = _need(status, np.uint8, P)
+    to = _need(tier_old, np.uint8, P)
+    nb = _need(nblk, np.uint32, P)
+    order_ = np.zeros(P, np.uint32)
+    prefix = np.zeros(P, np.uint64)
+    tier_new = np.zeros(P, np.uint8)
+    mg, mc = C.c_uint32(0), C.c_uint32(0)
+    rc = lib().orc_incremental(P, _ptr(it), _ptr(st), _ptr(to), _ptr(nb), int(block_bytes), int(gpu_budget),
+                               int(cpu_budget), flags, _ptr(order_), None, _ptr(prefix), _ptr(tier_new),
+                               C.byref(mg), C.byref(mc))
+    return rc, order_, prefix, tier_new, mg.value, mc.value
 
 
 @dataclass

@@ -71,3 +71,19 @@ def round_to_f32(fr: Fraction) -> np.float32:
     x = np.float32(float(fr))
     cands = [np.nextafter(x, np.float32(-np.inf)), x, np.nextafter(x, np.float32(np.inf))]
     return min(cands, key=lambda c: (abs(Fraction(float(c)) - fr), int(np.float32(c).view(np.uint32)) & 1))
+
+
+STATUS = {"R": 0, "A": 1, "N": 2}
+
+
+def incremental_cases():
+    sections, _ = _kv_blocks(os.path.join(GOLDEN, "incremental_worked.txt"))
+    res = {}
+    for name, kv in sections.items():
+        d = {k: [int(x) for x in kv[k].split()] for k in ("blocks", "tier", "new_tier", "order")}
+        d["status"] = [STATUS[x] for x in kv["status"].split()]
+        d["idleness"] = [float(x) for x in kv["idleness"].split()]
+        for key in ("gpu_budget", "cpu_budget", "skip_fit", "m_gpu", "m_cpu"):
+            d[key] = int(kv[key])
+        res[name] = d
+    return res
