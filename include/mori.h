@@ -75,7 +75,9 @@ extern "C" {
 #define MORI_DEV_NOSPC 0x100u         /* not enough pages (unreachable for a consistent pool) */
 #define MORI_DEV_HOST_ADDR 0x200u     /* swap address not 16-B aligned or outside registered memory */
 #define MORI_DEV_BAD_BLOCK 0x400u     /* eviction order: type label > 2 or last access >= 2^62 */
-/* classes: program data = 0x00F, pool state = 0x0F0, capacity = 0x100, swap = 0x200, blocks = 0x400 */
+#define MORI_DEV_BAD_STATUS 0x800u    /* incremental policy: status value > 2 */
+/* classes: program data = 0x00F and 0x800, pool state = 0x0F0, capacity = 0x100, swap = 0x200,
+   blocks = 0x400 */
 
 /* ---- tiers, table sentinel, flags, copy modes -------------------------- */
 #define MORI_TIER_GPU 0u
@@ -86,6 +88,12 @@ extern "C" {
 #define MORI_F_STATUS_KEY 1u     /* Acting programs (status 1) rank after all Reasoning ones */
 #define MORI_F_SKIP_FIT 2u       /* greedy fit in rank order instead of a strict prefix */
 #define MORI_F_IDLENESS_GIVEN 4u /* use programs.idleness instead of windows */
+#define MORI_F_INCREMENTAL 8u    /* incremental sticky policy of Sec. 4.3.1 instead of the boundary */
+
+/* program status (Sec. 4.1), read with MORI_F_STATUS_KEY or MORI_F_INCREMENTAL */
+#define MORI_ST_REASONING 0u /* running inference or waiting for it */
+#define MORI_ST_ACTING 1u    /* inside a tool call */
+#define MORI_ST_NEW 2u       /* newly arrived, waiting for its first inference (Reasoning elsewhere) */
 
 #define MORI_COPY_AUTO 0u   /* copy engines (chosen by measurement on MI355X) */
 #define MORI_COPY_KERNEL 1u /* kernels load/store host-mapped memory directly; no host sync */
@@ -123,7 +131,8 @@ typedef struct {
   const float* window;     /* device [P][window_k][2]: (reasoning s, acting s), oldest cycle
                               first; the newest acting entry is the ongoing call's elapsed time */
   const float* idleness;   /* device [P]; read only with MORI_F_IDLENESS_GIVEN */
-  const uint8_t* status;   /* device [P] 0 reasoning, 1 acting; read only with MORI_F_STATUS_KEY */
+  const uint8_t* status;   /* device [P] MORI_ST_*; read only with MORI_F_STATUS_KEY (where only
+                              MORI_ST_ACTING counts) or MORI_F_INCREMENTAL */
   const uint32_t* tbl_off; /* device [P+1] CSR offsets into tbl; nblk_p = tbl_off[p+1]-tbl_off[p] */
   uint32_t tbl_len;        /* entries allocated in tbl (>= tbl_off[P]) */
   uint32_t* tbl;           /* device [tbl_len], in/out: page id of each logical block of a
@@ -149,7 +158,7 @@ typedef struct {
   uint64_t pages_out, pages_in, pages_admit;
   uint64_t pages_free_before, pages_released, pages_recycled, pages_free_after;
   uint64_t bytes_out, bytes_in, gpu_bytes_after, cpu_bytes_after;
-  const uint32_t* order;        /* [P] program ids, busiest first */
+  const uint32_t* order;        /* [P] program ids, busiest first (incremental: see below) */
   const uint64_t* prefix;       /* [P] inclusive KV-byte prefix in rank order */
   const uint8_t* tier_old;      /* [P] */
   const uint8_t* tier_new;      /* [P] */
@@ -195,8 +204,34 @@ int mori_host_free(void* ptr);
 /* Computes the new placement and rewrites tbl, tier and free_map in stream
  * order.  Waits (on the stream) for the previous plan's swaps.  The plan is
  * copied to the context's pinned mirror; read it with mori_plan_wait.
- * EINVAL: null pointers, P > max_programs, window_k out of range, unknown
- * flags, gpu_bytes > num_blocks * block bytes. */
+ *
+ * Default policy (Sec. 4.3, Sec. 7.2): rank all programs by idleness (Eq. 1),
+ * busiest first, and fill the GPU tier, then the CPU tier, from the busiest
+ * end; a program moves only when it crosses a boundary.
+ *
+ * MORI_F_INCREMENTAL (Sec. 4.3.1; status required): tiers change only to
+ * repair a capacity violation or to fill free GPU room.  (1) While the CPU
+ * tier exceeds its budget, its programs go to Waiting in demotion order
+ * (Acting before Reasoning, highest idleness first, ties highest id first).
+ * (2) While the GPU tier exceeds its budget, the next program in demotion
+ * order leaves it, to the CPU tier if it fits in the CPU room left, else to
+ * Waiting; a Reasoning victim is demoted lazily: the caller lets its current
+ * inference step finish (orders it before the swap-out on the swap stream).
+ * (3) The GPU room left is filled from, in order: CPU programs waiting for
+ * inference, returning Waiting programs waiting for inference, new arrivals
+ * smallest context first; lowest idleness first within a level, ties lowest
+ * id.  Programs moved by (1)-(2) and Acting programs are no candidates; the
+ * walk stops at the first candidate that does not fit (MORI_F_SKIP_FIT:
+ * skips it).  Waiting programs are never placed on the CPU tier.  plan.order
+ * then lists programs by old tier -- GPU, CPU, then Waiting as returning,
+ * new (by context size), Acting -- each group by (Reasoning before Acting,
+ * idleness, id) or, for new arrivals, (context size, idleness, id); m_gpu and
+ * m_cpu count the programs on each tier afterwards.  A new arrival must have
+ * fewer than 2^31 blocks (MORI_DEV_BAD_TBL_OFF otherwise).
+ *
+ * EINVAL: null pointers (status with MORI_F_STATUS_KEY or MORI_F_INCREMENTAL),
+ * P > max_programs, window_k out of range, unknown flags, gpu_bytes >
+ * num_blocks * block bytes. */
 int mori_rank_partition(mori_ctx* ctx, const mori_programs* programs, const mori_budget* budget,
                         void* stream);
 

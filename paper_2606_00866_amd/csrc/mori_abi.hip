@@ -301,7 +301,8 @@ extern "C" int mori_rank_partition(mori_ctx* ctx, const mori_programs* pr, const
   if (!ctx || !pr || !b) return MORI_EINVAL;
   const uint32_t P = pr->num_programs;
   if (P > ctx->max_programs) return MORI_ENOSPC;
-  if (b->flags & ~(MORI_F_STATUS_KEY | MORI_F_SKIP_FIT | MORI_F_IDLENESS_GIVEN)) return MORI_EINVAL;
+  if (b->flags & ~(MORI_F_STATUS_KEY | MORI_F_SKIP_FIT | MORI_F_IDLENESS_GIVEN | MORI_F_INCREMENTAL))
+    return MORI_EINVAL;
   if (!pr->tbl_off || !pr->free_map) return MORI_EINVAL;
   if (P && (!pr->tier || (pr->tbl_len && !pr->tbl))) return MORI_EINVAL;
   if (b->flags & MORI_F_IDLENESS_GIVEN) {
@@ -310,7 +311,7 @@ extern "C" int mori_rank_partition(mori_ctx* ctx, const mori_programs* pr, const
     if (pr->window_k == 0 || pr->window_k > MORI_MAX_WINDOW) return MORI_EINVAL;
     if (P && !pr->window) return MORI_EINVAL;
   }
-  if ((b->flags & MORI_F_STATUS_KEY) && P && !pr->status) return MORI_EINVAL;
+  if ((b->flags & (MORI_F_STATUS_KEY | MORI_F_INCREMENTAL)) && P && !pr->status) return MORI_EINVAL;
   if (b->gpu_bytes > (uint64_t)ctx->pool.num_blocks * ctx->block_bytes) return MORI_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
   HIP_TRY(ctx, hipSetDevice(ctx->device));

@@ -2,14 +2,23 @@
 //
 //   1. idleness of every program by Eq. 1 (Sec. 4.2), binary32, totals
 //      accumulated oldest cycle first from +0, correctly rounded division;
-//   2. a 32-bit key per program (idleness bits, optionally the Acting bit of
-//      the demotion order of Sec. 4.3.1) and a stable LSD radix sort of
-//      (key, id) with wave64 ballots -- the relative ranking, busiest first;
-//   3. an inclusive u64 scan of KV bytes in rank order and the two
+//   2. a 64-bit key per program and a stable LSD radix sort of (key, id) with
+//      wave64 ballots.  Boundary policy: the key is the idleness bits,
+//      optionally with the Acting bit of the demotion order of Sec. 4.3.1 --
+//      the relative ranking, busiest first.  Incremental policy (Sec. 4.3.1):
+//      the key is the program's listing group (old tier; Waiting split into
+//      returning, new and Acting) above its priority in that group, so each
+//      tier group lists its programs in reverse demotion order and the
+//      promotion candidates come in promotion order;
+//   3. an inclusive u64 scan of KV bytes in that order, then either the two
 //      capacity boundaries (Sec. 4.1 per-tier capacity, Sec. 7.2 fill from the
-//      busiest end), or the greedy skip-fit walk;
+//      busiest end) or the greedy skip-fit walk, or the incremental policy:
+//      demote-until-fits is the tail of a tier group past its longest fitting
+//      prefix, promote-while-fits a prefix of the candidates' byte scan;
+//      victims that do not all fit the CPU room and skip-fit promotion are
+//      walked one by one by one thread;
 //   4. the sticky diff (Sec. 4.3): per-program transition category, the
-//      swap-out and swap-in lists in rank order and the page/slot bases.
+//      swap-out and swap-in lists in that order and the page/slot bases.
 //
 // P <= 4096 programs fit in LDS (4 keys per thread), so the whole step is one
 // launch of a few microseconds; nothing here is bandwidth-bound.
@@ -23,6 +32,8 @@ constexpr int IPT = 4;             // items per thread, striped: item x = it * R
 constexpr int NW = RT / 64;        // wavefronts
 constexpr int RADIX_BITS = 4;
 constexpr int RADIX = 1 << RADIX_BITS;
+constexpr int KEY_BITS = 64;
+constexpr int GROUP_SHIFT = 61;  // incremental keys: listing group in the top three bits
 static_assert(RT * IPT == (int)MORI_MAX_PROGRAMS, "one key per thread slot");
 static_assert(RADIX * IPT * NW == RT, "one digit counter per thread");
 
@@ -65,23 +76,28 @@ __device__ inline uint8_t category(uint8_t from, uint8_t to) {
 }
 
 __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
-  __shared__ uint32_t s_key[RT * IPT];
-  __shared__ uint32_t s_id[RT * IPT];
+  __shared__ uint64_t s_key[RT * IPT];  // sort scratch, then the inclusive byte prefix by rank
+  __shared__ uint32_t s_id[RT * IPT];   // sort scratch, then blocks by rank
   __shared__ uint32_t s_cnt[RT];
   __shared__ uint8_t s_tier[RT * IPT];
   __shared__ uint64_t s_w64[NW + 1];
   __shared__ uint32_t s_w32[NW + 1];
-  __shared__ uint32_t s_err, s_or, s_and, s_m_gpu, s_m_cpu;
+  __shared__ unsigned long long s_or, s_and;
+  __shared__ uint32_t s_err, s_m_gpu, s_m_cpu;
+  __shared__ uint32_t s_grp[5], s_cpu_reasoning, s_k_gpu, s_k_cpu;
   __shared__ uint32_t s_n_drop_gpu, s_n_drop_cpu, s_n_admit_gpu, s_n_admit_cpu;
   __shared__ unsigned long long s_gpu_after, s_cpu_after, s_gpu_part;
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const uint32_t P = a.P;
+  const bool incremental = (a.flags & MORI_F_INCREMENTAL) != 0;
   if (tid == 0) {
     s_err = 0;
     s_or = 0;
-    s_and = 0xFFFFFFFFu;
+    s_and = ~0ull;
     s_m_gpu = s_m_cpu = 0;
+    for (int g = 0; g < 5; ++g) s_grp[g] = 0;
+    s_cpu_reasoning = s_k_gpu = s_k_cpu = 0;
     s_n_drop_gpu = s_n_drop_cpu = s_n_admit_gpu = s_n_admit_cpu = 0;
     s_gpu_after = s_cpu_after = 0;
     s_gpu_part = 0;
@@ -93,20 +109,24 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
   __syncthreads();
 
   // ---- 1. validation, Eq. 1, keys --------------------------------------
-  uint32_t key[IPT], id[IPT];
+  uint64_t key[IPT];
+  uint32_t id[IPT];
   uint32_t err = 0;
   if (tid == 0) {
     if (a.tbl_off[0] != 0u) err |= MORI_DEV_BAD_TBL_OFF;
     if (a.tbl_off[P] > a.tbl_len) err |= MORI_DEV_BAD_TBL_OFF;
   }
+  unsigned long long k_or = 0, k_and = ~0ull;
 #pragma unroll
   for (int it = 0; it < IPT; ++it) {
     const uint32_t x = it * RT + tid;
-    key[it] = 0xFFFFFFFFu;  // padding sorts after every real key
+    key[it] = ~0ull;  // padding sorts after every real key
     id[it] = x;
     if (x >= P) continue;
-    if (a.tier[x] > MORI_TIER_WAIT) err |= MORI_DEV_BAD_TIER;
-    if (a.tbl_off[x + 1] < a.tbl_off[x]) err |= MORI_DEV_BAD_TBL_OFF;
+    const uint8_t told = a.tier[x];
+    const uint32_t off0 = a.tbl_off[x], off1 = a.tbl_off[x + 1];
+    if (told > MORI_TIER_WAIT) err |= MORI_DEV_BAD_TIER;
+    if (off1 < off0) err |= MORI_DEV_BAD_TBL_OFF;
     float v;
     if (a.flags & MORI_F_IDLENESS_GIVEN) {
       v = a.idleness[x];
@@ -126,12 +146,36 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
       v = (total > 0.0f) ? t_acting / total : 0.0f;
     }
     if (v == 0.0f) v = 0.0f;  // a negative zero keys like +0
-    uint32_t bits = __float_as_uint(v);
-    if ((a.flags & MORI_F_STATUS_KEY) && a.status[x] == 1) bits |= 0x80000000u;
-    key[it] = bits;
-    atomicOr(&s_or, bits);
-    atomicAnd(&s_and, bits);
+    const uint32_t bits = __float_as_uint(v);  // < 2^30 for idleness in [0, 1]
+    uint64_t k;
+    if (incremental) {
+      const uint8_t st = a.status[x];
+      if (st > MORI_ST_NEW) err |= MORI_DEV_BAD_STATUS;
+      const uint64_t acting = st == MORI_ST_ACTING;
+      uint64_t grp;
+      uint64_t sub = bits;
+      if (told == MORI_TIER_GPU || told == MORI_TIER_CPU) {
+        grp = told;  // Reasoning before Acting, then idleness: the reverse of the demotion order
+        sub |= acting << 31;
+      } else if (st == MORI_ST_NEW) {
+        grp = 3;  // new arrivals: smallest context first
+        const uint32_t nb = off1 - off0;
+        if (nb >= 0x80000000u) err |= MORI_DEV_BAD_TBL_OFF;
+        sub |= (uint64_t)nb << 30;
+      } else {
+        grp = acting ? 4 : 2;
+      }
+      k = (grp << GROUP_SHIFT) | sub;
+    } else {
+      k = bits;
+      if ((a.flags & MORI_F_STATUS_KEY) && a.status[x] == MORI_ST_ACTING) k |= 0x80000000u;
+    }
+    key[it] = k;
+    k_or |= k;
+    k_and &= k;
   }
+  if (k_or) atomicOr(&s_or, k_or);
+  if (k_and != ~0ull) atomicAnd(&s_and, k_and);
   if (err) atomicOr(&s_err, err);
   __syncthreads();
   if (s_err) {
@@ -144,16 +188,16 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
   // them in thread order gives every (digit, item slice, wave) its output base
   // in (digit, original position) order, i.e. a stable pass.  Digits on which
   // every real key agrees are skipped; padding keeps the tail.
-  const uint32_t varying = s_or ^ s_and;
+  const uint64_t varying = s_or ^ s_and;
   const uint64_t lanemask_lt = (1ull << lane) - 1ull;
-  for (int shift = 0; shift < 32; shift += RADIX_BITS) {
+  for (int shift = 0; shift < KEY_BITS; shift += RADIX_BITS) {
     if (((varying >> shift) & (RADIX - 1)) == 0) continue;
     uint32_t digit[IPT], lrank[IPT];
     s_cnt[tid] = 0;
     __syncthreads();
 #pragma unroll
     for (int it = 0; it < IPT; ++it) {
-      const uint32_t d = (key[it] >> shift) & (RADIX - 1);
+      const uint32_t d = (uint32_t)(key[it] >> shift) & (RADIX - 1);
       uint64_t same = ~0ull;
 #pragma unroll
       for (int b = 0; b < RADIX_BITS; ++b) {
@@ -194,9 +238,10 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
       a.order[r] = id[it];
       nb[it] = a.tbl_off[id[it] + 1] - a.tbl_off[id[it]];
     }
+    s_id[r] = nb[it];
   }
 
-  // ---- 3. KV-byte prefix in rank order and the boundaries ---------------
+  // ---- 3. KV-byte prefix in that order and the placement ----------------
   uint64_t S[IPT];
   uint64_t carry = 0;
 #pragma unroll
@@ -207,9 +252,107 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     S[it] = carry + ex + bytes;
     carry += tot;
     const uint32_t r = it * RT + tid;
+    s_key[r] = S[it];
     if (r < P) a.prefix[r] = S[it];
   }
-  if (!(a.flags & MORI_F_SKIP_FIT)) {
+  if (incremental) {
+    // listing groups: [0, g1) GPU, [g1, g2) CPU, [g2, g3) Waiting returning,
+    // [g3, g4) new arrivals, [g4, P) Waiting Acting
+#pragma unroll
+    for (int it = 0; it < IPT; ++it) {
+      const uint32_t r = it * RT + tid;
+      if (r >= P) continue;
+      const uint32_t g = (uint32_t)(key[it] >> GROUP_SHIFT);
+      atomicAdd(&s_grp[g], 1u);
+      if (g == MORI_TIER_CPU && !((key[it] >> 31) & 1u)) atomicAdd(&s_cpu_reasoning, 1u);
+    }
+    __syncthreads();
+    const uint32_t g1 = s_grp[0], g2 = g1 + s_grp[1], g3 = g2 + s_grp[2], g4 = g3 + s_grp[3];
+    const uint64_t gpu_total = g1 ? s_key[g1 - 1] : 0;
+    // (1) CPU admission control and (2) demotion from GPU: each tier keeps the
+    // longest prefix of its group that fits its budget (the rest, in reverse,
+    // is the demotion order's shortest prefix whose removal fits)
+    uint32_t kg = 0, kc = 0;
+#pragma unroll
+    for (int it = 0; it < IPT; ++it) {
+      const uint32_t r = it * RT + tid;
+      if (r < g1 && S[it] <= a.gpu_bytes) ++kg;
+      if (r >= g1 && r < g2 && S[it] - gpu_total <= a.cpu_bytes) ++kc;
+    }
+    if (kg) atomicAdd(&s_k_gpu, kg);
+    if (kc) atomicAdd(&s_k_cpu, kc);
+    __syncthreads();
+    const uint32_t k_gpu = s_k_gpu, k_cpu = s_k_cpu;
+    const uint64_t gpu_kept = k_gpu ? s_key[k_gpu - 1] : 0;
+    const uint64_t cpu_kept = k_cpu ? s_key[g1 + k_cpu - 1] - gpu_total : 0;
+    const uint64_t room_cpu = a.cpu_bytes - cpu_kept;
+    const uint64_t room_gpu = a.gpu_bytes - gpu_kept;
+    const bool victims_fit = gpu_total - gpu_kept <= room_cpu;
+    const uint32_t c_end = g1 + min(k_cpu, s_cpu_reasoning);  // CPU candidates: [g1, c_end)
+#pragma unroll
+    for (int it = 0; it < IPT; ++it) {
+      const uint32_t r = it * RT + tid;
+      uint8_t t;
+      if (r < k_gpu) t = MORI_TIER_GPU;
+      else if (r < g1) t = victims_fit ? MORI_TIER_CPU : MORI_TIER_WAIT;  // else walked below
+      else if (r < g1 + k_cpu) t = MORI_TIER_CPU;
+      else t = MORI_TIER_WAIT;
+      s_tier[r] = t;
+    }
+    // (3) promotion: a strict prefix of the candidates' byte scan
+    if (!(a.flags & MORI_F_SKIP_FIT)) {
+      uint64_t ccarry = 0;
+#pragma unroll
+      for (int it = 0; it < IPT; ++it) {
+        const uint32_t r = it * RT + tid;
+        const bool cand = (r >= g1 && r < c_end) || (r >= g2 && r < g4);
+        const uint64_t cb = cand ? (uint64_t)nb[it] * a.block_bytes : 0;
+        uint64_t tot;
+        const uint64_t T = ccarry + block_scan_excl<uint64_t>(cb, s_w64, &tot) + cb;
+        ccarry += tot;
+        if (cand && T <= room_gpu) s_tier[r] = MORI_TIER_GPU;
+      }
+    }
+    __syncthreads();
+    if (tid == 0) {
+      if (!victims_fit) {  // each victim, most demotable first, to the CPU tier if it still fits
+        uint64_t room = room_cpu;
+        for (uint32_t r = g1; r-- > k_gpu;) {
+          const uint64_t b = (uint64_t)s_id[r] * a.block_bytes;
+          if (b <= room) {
+            room -= b;
+            s_tier[r] = MORI_TIER_CPU;
+          } else {
+            s_tier[r] = MORI_TIER_WAIT;
+          }
+        }
+      }
+      if (a.flags & MORI_F_SKIP_FIT) {
+        uint64_t room = room_gpu;
+        for (int part = 0; part < 2; ++part) {
+          const uint32_t lo = part ? g2 : g1, hi = part ? g4 : c_end;
+          for (uint32_t r = lo; r < hi; ++r) {
+            const uint64_t b = (uint64_t)s_id[r] * a.block_bytes;
+            if (b <= room) {
+              room -= b;
+              s_tier[r] = MORI_TIER_GPU;
+            }
+          }
+        }
+      }
+    }
+    __syncthreads();
+    uint32_t ng = 0, nc = 0;
+#pragma unroll
+    for (int it = 0; it < IPT; ++it) {
+      const uint32_t r = it * RT + tid;
+      if (r >= P) continue;
+      ng += s_tier[r] == MORI_TIER_GPU;
+      nc += s_tier[r] == MORI_TIER_CPU;
+    }
+    if (ng) atomicAdd(&s_m_gpu, ng);
+    if (nc) atomicAdd(&s_m_cpu, nc);
+  } else if (!(a.flags & MORI_F_SKIP_FIT)) {
     // S is non-decreasing in rank order, so the longest feasible prefix is
     // the number of ranks whose inclusive prefix fits the budget.
     uint32_t c = 0;
@@ -240,14 +383,12 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     }
   } else {
     // Greedy walk in rank order: first tier that still has room.
-#pragma unroll
-    for (int it = 0; it < IPT; ++it) s_key[it * RT + tid] = nb[it];
     __syncthreads();
     if (tid == 0) {
       uint64_t room_gpu = a.gpu_bytes, room_cpu = a.cpu_bytes;
       uint32_t ng = 0, nc = 0;
       for (uint32_t r = 0; r < P; ++r) {
-        const uint64_t bytes = (uint64_t)s_key[r] * a.block_bytes;
+        const uint64_t bytes = (uint64_t)s_id[r] * a.block_bytes;
         if (bytes <= room_gpu) {
           room_gpu -= bytes;
           s_tier[r] = MORI_TIER_GPU;

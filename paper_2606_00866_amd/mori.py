@@ -16,11 +16,12 @@ LIB_PATH = os.path.join(HERE, "libmori.so")
 MORI_OK, MORI_EINVAL, MORI_ENOSPC, MORI_ESTATE, MORI_EHIP, MORI_EDEVICE = 0, -1, -2, -3, -4, -5
 MORI_DEV_BAD_WINDOW, MORI_DEV_BAD_IDLENESS, MORI_DEV_BAD_TIER, MORI_DEV_BAD_TBL_OFF = 0x1, 0x2, 0x4, 0x8
 MORI_DEV_PAGE_RANGE, MORI_DEV_PAGE_DUP, MORI_DEV_PAGE_LEAK, MORI_DEV_NONRES_PAGE = 0x10, 0x20, 0x40, 0x80
-MORI_DEV_NOSPC, MORI_DEV_HOST_ADDR, MORI_DEV_BAD_BLOCK = 0x100, 0x200, 0x400
+MORI_DEV_NOSPC, MORI_DEV_HOST_ADDR, MORI_DEV_BAD_BLOCK, MORI_DEV_BAD_STATUS = 0x100, 0x200, 0x400, 0x800
 MORI_TYPE_BUSY, MORI_TYPE_IDLE, MORI_TYPE_INACTIVE = 0, 1, 2
 MORI_TIER_GPU, MORI_TIER_CPU, MORI_TIER_WAIT = 0, 1, 2
 MORI_NO_PAGE = 0xFFFFFFFF
-MORI_F_STATUS_KEY, MORI_F_SKIP_FIT, MORI_F_IDLENESS_GIVEN = 1, 2, 4
+MORI_F_STATUS_KEY, MORI_F_SKIP_FIT, MORI_F_IDLENESS_GIVEN, MORI_F_INCREMENTAL = 1, 2, 4, 8
+MORI_ST_REASONING, MORI_ST_ACTING, MORI_ST_NEW = 0, 1, 2
 MORI_COPY_AUTO, MORI_COPY_KERNEL, MORI_COPY_CE = 0, 1, 2
 (MORI_CAT_KEPT, MORI_CAT_OUT, MORI_CAT_IN, MORI_CAT_DROP_GPU, MORI_CAT_DROP_CPU, MORI_CAT_ADMIT_GPU,
  MORI_CAT_ADMIT_CPU) = range(7)

@@ -100,3 +100,13 @@ def test_host_side_argument_errors():
     assert M.mori_evict_order(blk, 0, 0, ws.data_ptr(), w - 8, o.data_ptr(), 0, res.data_ptr()) == M.MORI_EINVAL
     assert M.mori_evict_order(blk, 0, 0, ws.data_ptr() + 8, w, o.data_ptr(), 0, res.data_ptr()) == M.MORI_EINVAL
     assert M.mori_evict_order(blk, 0, 0, ws.data_ptr(), w, 0, 0, res.data_ptr()) == M.MORI_EINVAL
+
+
+@pytest.mark.parametrize("N", [69938, 1 << 20])
+def test_bench_inputs(N):
+    """The eviction-order leg of bench.py times these exact inputs."""
+    import bench
+
+    typ, la, size, need = bench.evict_inputs(np, N)
+    log(f"evict bench inputs N={N}")
+    check(typ, la, size, 4096, 0, need)
