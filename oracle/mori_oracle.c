@@ -106,16 +106,17 @@ void orc_order(uint32_t P, const uint32_t* key, uint32_t* order, uint32_t* rank)
 /* the ranking once and puts each program in the first tier it still fits.  */
 /* ------------------------------------------------------------------------ */
 void orc_boundary(uint32_t P, const uint32_t* order, const uint32_t* nblk, uint64_t block_bytes,
-                  uint64_t gpu_budget, uint64_t cpu_budget, uint32_t flags, uint64_t* prefix,
-                  uint8_t* tier_new, uint32_t* m_gpu, uint32_t* m_cpu) {
+                  uint64_t gpu_budget, uint64_t cpu_budget, uint64_t ssd_budget, uint32_t flags,
+                  uint64_t* prefix, uint8_t* tier_new, uint32_t* m_gpu, uint32_t* m_cpu, uint32_t* m_ssd) {
+  const int ssd = (flags & ORC_F_SSD_TIER) != 0;
   uint64_t running = 0;
   for (uint32_t r = 0; r < P; ++r) {
     running += (uint64_t)nblk[order[r]] * block_bytes;
     prefix[r] = running;
   }
-  uint32_t n_gpu = 0, n_cpu = 0;
+  uint32_t n_gpu = 0, n_cpu = 0, n_ssd = 0;
   if (flags & ORC_F_SKIP_FIT) {
-    uint64_t room_gpu = gpu_budget, room_cpu = cpu_budget;
+    uint64_t room_gpu = gpu_budget, room_cpu = cpu_budget, room_ssd = ssd_budget;
     for (uint32_t r = 0; r < P; ++r) {
       uint32_t p = order[r];
       uint64_t bytes = (uint64_t)nblk[p] * block_bytes;
@@ -127,6 +128,10 @@ void orc_boundary(uint32_t P, const uint32_t* order, const uint32_t* nblk, uint6
         room_cpu -= bytes;
         tier_new[p] = ORC_CPU;
         ++n_cpu;
+      } else if (ssd && bytes <= room_ssd) {
+        room_ssd -= bytes;
+        tier_new[p] = ORC_SSD;
+        ++n_ssd;
       } else {
         tier_new[p] = ORC_WAIT;
       }
@@ -135,20 +140,33 @@ void orc_boundary(uint32_t P, const uint32_t* order, const uint32_t* nblk, uint6
     while (n_gpu < P && prefix[n_gpu] <= gpu_budget) ++n_gpu;
     uint64_t gpu_part = n_gpu ? prefix[n_gpu - 1] : 0;
     while (n_gpu + n_cpu < P && prefix[n_gpu + n_cpu] - gpu_part <= cpu_budget) ++n_cpu;
+    if (ssd) { /* Sec. 7.1: the programs between the second and a third threshold go to SSD */
+      uint64_t upper_part = (n_gpu + n_cpu) ? prefix[n_gpu + n_cpu - 1] : 0;
+      while (n_gpu + n_cpu + n_ssd < P && prefix[n_gpu + n_cpu + n_ssd] - upper_part <= ssd_budget) ++n_ssd;
+    }
     for (uint32_t r = 0; r < P; ++r) {
       uint32_t p = order[r];
-      tier_new[p] = (r < n_gpu) ? ORC_GPU : (r < n_gpu + n_cpu) ? ORC_CPU : ORC_WAIT;
+      tier_new[p] = (r < n_gpu) ? ORC_GPU
+                  : (r < n_gpu + n_cpu) ? ORC_CPU
+                  : (r < n_gpu + n_cpu + n_ssd) ? ORC_SSD : ORC_WAIT;
     }
   }
   *m_gpu = n_gpu;
   *m_cpu = n_cpu;
+  *m_ssd = n_ssd;
 }
 
+/* Transition category, old tier -> new tier.  Leaving the GPU for a lower
+   tier that keeps the KV (CPU, SSD) is a swap-out, the reverse a swap-in. */
 static uint8_t orc_category(uint8_t from, uint8_t to) {
-  if (from == to) return ORC_KEPT;
-  if (from == ORC_GPU) return to == ORC_CPU ? ORC_OUT : ORC_DROP_GPU;
-  if (from == ORC_CPU) return to == ORC_GPU ? ORC_IN : ORC_DROP_CPU;
-  return to == ORC_GPU ? ORC_ADMIT_GPU : ORC_ADMIT_CPU;
+  static const uint8_t table[4][4] = {
+      /* to:           GPU            CPU            WAIT           SSD */
+      /* GPU  */ {ORC_KEPT, ORC_OUT, ORC_DROP_GPU, ORC_OUT},
+      /* CPU  */ {ORC_IN, ORC_KEPT, ORC_DROP_CPU, ORC_CPU_SSD},
+      /* WAIT */ {ORC_ADMIT_GPU, ORC_ADMIT_CPU, ORC_KEPT, ORC_ADMIT_SSD},
+      /* SSD  */ {ORC_IN, ORC_SSD_CPU, ORC_DROP_SSD, ORC_KEPT},
+  };
+  return table[from][to];
 }
 
 /* ------------------------------------------------------------------------ */
@@ -322,7 +340,7 @@ int orc_incremental(uint32_t P, const float* iota_in, const uint8_t* status, con
 int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32_t k,
                   const float* window, const float* iota_given, const uint8_t* status,
                   const uint32_t* tbl_off, uint32_t tbl_len, uint32_t* tbl, uint8_t* tier,
-                  uint8_t* free_map, uint64_t gpu_budget, uint64_t cpu_budget, uint32_t flags,
+                  uint8_t* free_map, uint64_t gpu_budget, uint64_t cpu_budget, uint64_t ssd_budget, uint32_t flags,
                   uint8_t* const* host_bufs, uint32_t* order_out, uint32_t* rank_out,
                   uint8_t* tier_old_out, uint8_t* category_out, uint64_t* prefix_out,
                   orc_summary* summary) {
@@ -346,8 +364,10 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
   uint32_t* new_tbl = NULL;
 
   /* -- program data: tiers and the block-table offsets -- */
+  const uint8_t top_tier = (flags & ORC_F_SSD_TIER) ? ORC_SSD : ORC_WAIT;
+  if ((flags & ORC_F_SSD_TIER) && (flags & ORC_F_INCREMENTAL)) rc = ORC_E_INPUT;
   for (uint32_t p = 0; p < P && rc == ORC_OK; ++p)
-    if (tier[p] > ORC_WAIT) rc = ORC_E_INPUT;
+    if (tier[p] > top_tier) rc = ORC_E_INPUT;
   if (rc == ORC_OK && tbl_off[0] != 0) rc = ORC_E_INPUT;
   for (uint32_t p = 0; p < P && rc == ORC_OK; ++p) {
     if (tbl_off[p + 1] < tbl_off[p]) rc = ORC_E_INPUT;
@@ -363,7 +383,7 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
       rc = orc_idleness(P, k, window, iota);
     }
   }
-  uint32_t m_gpu = 0, m_cpu = 0;
+  uint32_t m_gpu = 0, m_cpu = 0, m_ssd = 0;
   if (rc == ORC_OK && (flags & ORC_F_INCREMENTAL)) {
     if (status == NULL && P) rc = ORC_E_INPUT;
     else rc = orc_incremental(P, iota, status, tier, nblk, block_bytes, gpu_budget, cpu_budget, flags, order,
@@ -372,8 +392,8 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
     rc = orc_keys(P, iota, status, flags, key);
     if (rc == ORC_OK) {
       orc_order(P, key, order, rank);
-      orc_boundary(P, order, nblk, block_bytes, gpu_budget, cpu_budget, flags, prefix, tier_new,
-                   &m_gpu, &m_cpu);
+      orc_boundary(P, order, nblk, block_bytes, gpu_budget, cpu_budget, ssd_budget, flags, prefix, tier_new,
+                   &m_gpu, &m_cpu, &m_ssd);
     }
   }
   if (rc == ORC_OK)
@@ -470,6 +490,7 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
       memset(summary, 0, sizeof *summary);
       summary->m_gpu = m_gpu;
       summary->m_cpu = m_cpu;
+      summary->m_ssd = m_ssd;
       for (uint32_t p = 0; p < P; ++p) {
         uint64_t pages = nblk[p];
         switch (cat[p]) {
@@ -483,6 +504,7 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
         }
         if (tier_new[p] == ORC_GPU) summary->gpu_bytes_after += pages * block_bytes;
         if (tier_new[p] == ORC_CPU) summary->cpu_bytes_after += pages * block_bytes;
+        if (tier_new[p] == ORC_SSD) summary->ssd_bytes_after += pages * block_bytes;
       }
       summary->pages_free_before = n_free0;
       summary->pages_released = n_rel;

@@ -34,10 +34,12 @@
 extern "C" {
 #endif
 
-/* tiers (Sec. 4.1: GPU queue, CPU queue, Waiting queue) */
+/* tiers (Sec. 4.1: GPU queue, CPU queue, Waiting queue; Sec. 7.1: an SSD
+   tier below the CPU tier) */
 #define ORC_GPU 0u
 #define ORC_CPU 1u
 #define ORC_WAIT 2u
+#define ORC_SSD 3u
 #define ORC_NONE 0xFFFFFFFFu /* table entry of a block that has no HBM page */
 
 /* flags */
@@ -45,6 +47,7 @@ extern "C" {
 #define ORC_F_SKIP_FIT 2u       /* greedy fit instead of a strict prefix boundary */
 #define ORC_F_IDLENESS_GIVEN 4u /* idleness supplied directly instead of windows */
 #define ORC_F_INCREMENTAL 8u    /* incremental sticky policy (Sec. 4.3.1) instead of the boundary */
+#define ORC_F_SSD_TIER 16u      /* a third boundary: SSD tier after the CPU tier (Sec. 7.1) */
 
 /* program status (Sec. 4.1): Reasoning = running or waiting for inference,
    Acting = inside a tool call, New = arrived and not yet run (waits for its
@@ -61,23 +64,27 @@ extern "C" {
 
 /* transition categories, old tier -> new tier */
 #define ORC_KEPT 0u
-#define ORC_OUT 1u       /* GPU -> CPU: swap-out */
-#define ORC_IN 2u        /* CPU -> GPU: swap-in */
+#define ORC_OUT 1u       /* GPU -> CPU or SSD: swap-out into the program's host buffer */
+#define ORC_IN 2u        /* CPU or SSD -> GPU: swap-in from the program's host buffer */
 #define ORC_DROP_GPU 3u  /* GPU -> WAIT: pages released, KV discarded */
 #define ORC_DROP_CPU 4u  /* CPU -> WAIT */
 #define ORC_ADMIT_GPU 5u /* WAIT -> GPU: pages reserved, no copy (prefill recomputes) */
 #define ORC_ADMIT_CPU 6u /* WAIT -> CPU */
+#define ORC_CPU_SSD 7u   /* CPU -> SSD: host buffer written to storage, no GPU work */
+#define ORC_SSD_CPU 8u   /* SSD -> CPU */
+#define ORC_DROP_SSD 9u  /* SSD -> WAIT */
+#define ORC_ADMIT_SSD 10u /* WAIT -> SSD */
 
 typedef struct {
   uint32_t layers, planes, block_tokens, row_bytes, num_blocks;
 } orc_geometry;
 
 typedef struct {
-  uint32_t m_gpu, m_cpu;
+  uint32_t m_gpu, m_cpu, m_ssd;
   uint32_t n_out, n_in, n_drop_gpu, n_drop_cpu, n_admit_gpu, n_admit_cpu;
   uint64_t pages_out, pages_in, pages_admit;
   uint64_t pages_free_before, pages_released, pages_recycled, pages_free_after;
-  uint64_t bytes_out, bytes_in, gpu_bytes_after, cpu_bytes_after;
+  uint64_t bytes_out, bytes_in, gpu_bytes_after, cpu_bytes_after, ssd_bytes_after;
 } orc_summary;
 
 /* Eq. 1 for every program.  window is [P][k][2] (reasoning s, acting s), oldest first. */
@@ -90,10 +97,11 @@ int orc_keys(uint32_t P, const float* iota, const uint8_t* status, uint32_t flag
 void orc_order(uint32_t P, const uint32_t* key, uint32_t* order, uint32_t* rank);
 
 /* Capacity-matched boundary over the ranking.  prefix[r] = KV bytes of the
- * first r+1 programs in rank order. */
+ * first r+1 programs in rank order.  With ORC_F_SSD_TIER a third run after the
+ * CPU tier's goes to the SSD tier (ssd_budget, m_ssd); otherwise m_ssd = 0. */
 void orc_boundary(uint32_t P, const uint32_t* order, const uint32_t* nblk, uint64_t block_bytes,
-                  uint64_t gpu_budget, uint64_t cpu_budget, uint32_t flags, uint64_t* prefix,
-                  uint8_t* tier_new, uint32_t* m_gpu, uint32_t* m_cpu);
+                  uint64_t gpu_budget, uint64_t cpu_budget, uint64_t ssd_budget, uint32_t flags,
+                  uint64_t* prefix, uint8_t* tier_new, uint32_t* m_gpu, uint32_t* m_cpu, uint32_t* m_ssd);
 
 /* Incremental sticky placement (Sec. 4.3 and Sec. 4.3.1), the alternative to
  * the boundary: tiers change only to repair a capacity violation or to fill
@@ -131,11 +139,14 @@ int orc_incremental(uint32_t P, const float* iota, const uint8_t* status, const 
  * program) may both be NULL to compute the placement only.
  * Optional outputs (may be NULL): order, rank, tier_old_out, category, prefix, summary.
  * With ORC_F_INCREMENTAL the placement comes from orc_incremental (status
- * required) instead of the ranking and boundary. */
+ * required) instead of the ranking and boundary.  With ORC_F_SSD_TIER tier 3
+ * (SSD) is a valid tier, the boundary has a third run (ssd_budget), and an SSD
+ * program's KV lives in its host buffer as a CPU program's does (the storage
+ * I/O is the caller's); ORC_F_SSD_TIER with ORC_F_INCREMENTAL is rejected. */
 int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32_t k,
                   const float* window, const float* iota_given, const uint8_t* status,
                   const uint32_t* tbl_off, uint32_t tbl_len, uint32_t* tbl, uint8_t* tier,
-                  uint8_t* free_map, uint64_t gpu_budget, uint64_t cpu_budget, uint32_t flags,
+                  uint8_t* free_map, uint64_t gpu_budget, uint64_t cpu_budget, uint64_t ssd_budget, uint32_t flags,
                   uint8_t* const* host_bufs, uint32_t* order, uint32_t* rank, uint8_t* tier_old_out,
                   uint8_t* category, uint64_t* prefix, orc_summary* summary);
 

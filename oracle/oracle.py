@@ -21,13 +21,13 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "mori_oracle.c")
 LIB = os.path.join(HERE, "liboracle.so")
 
-GPU, CPU, WAIT = 0, 1, 2
+GPU, CPU, WAIT, SSD = 0, 1, 2, 3
 TYPE_BUSY, TYPE_IDLE, TYPE_INACTIVE = 0, 1, 2
 NONE = 0xFFFFFFFF
-F_STATUS_KEY, F_SKIP_FIT, F_IDLENESS_GIVEN, F_INCREMENTAL = 1, 2, 4, 8
+F_STATUS_KEY, F_SKIP_FIT, F_IDLENESS_GIVEN, F_INCREMENTAL, F_SSD_TIER = 1, 2, 4, 8, 16
 ST_REASONING, ST_ACTING, ST_NEW = 0, 1, 2
 OK, E_INPUT, E_POOL, E_NOSPC = 0, 1, 2, 3
-KEPT, OUT, IN, DROP_GPU, DROP_CPU, ADMIT_GPU, ADMIT_CPU = range(7)
+KEPT, OUT, IN, DROP_GPU, DROP_CPU, ADMIT_GPU, ADMIT_CPU, CPU_SSD, SSD_CPU, DROP_SSD, ADMIT_SSD = range(11)
 
 
 def build(force: bool = False) -> str:
@@ -50,11 +50,11 @@ class _Geometry(C.Structure):
 
 class _Summary(C.Structure):
     _fields_ = [(n, C.c_uint32) for n in (
-        "m_gpu", "m_cpu", "n_out", "n_in", "n_drop_gpu", "n_drop_cpu", "n_admit_gpu", "n_admit_cpu")] + [
+        "m_gpu", "m_cpu", "m_ssd", "n_out", "n_in", "n_drop_gpu", "n_drop_cpu", "n_admit_gpu", "n_admit_cpu")] + [
         (n, C.c_uint64) for n in (
             "pages_out", "pages_in", "pages_admit", "pages_free_before", "pages_released",
             "pages_recycled", "pages_free_after", "bytes_out", "bytes_in", "gpu_bytes_after",
-            "cpu_bytes_after")]
+            "cpu_bytes_after", "ssd_bytes_after")]
 
 
 _lib = None
@@ -69,11 +69,11 @@ def lib():
         _lib.orc_keys.argtypes = [C.c_uint32, P, P, C.c_uint32, P]
         _lib.orc_order.argtypes = [C.c_uint32, P, P, P]
         _lib.orc_order.restype = None
-        _lib.orc_boundary.argtypes = [C.c_uint32, P, P, C.c_uint64, C.c_uint64, C.c_uint64, C.c_uint32,
-                                      P, P, P, P]
+        _lib.orc_boundary.argtypes = [C.c_uint32, P, P, C.c_uint64, C.c_uint64, C.c_uint64, C.c_uint64,
+                                      C.c_uint32, P, P, P, P, P]
         _lib.orc_boundary.restype = None
         _lib.orc_rebalance.argtypes = [P, P, C.c_uint32, C.c_uint32, P, P, P, P, C.c_uint32, P, P, P,
-                                       C.c_uint64, C.c_uint64, C.c_uint32, P, P, P, P, P, P, P]
+                                       C.c_uint64, C.c_uint64, C.c_uint64, C.c_uint32, P, P, P, P, P, P, P]
         _lib.orc_incremental.argtypes = [C.c_uint32, P, P, P, P, C.c_uint64, C.c_uint64, C.c_uint64, C.c_uint32,
                                          P, P, P, P, P, P]
         _lib.orc_evict_order.argtypes = [C.c_uint32, P, P, P, C.c_uint64, C.c_uint32, C.c_uint64, P, P, P]
@@ -116,15 +116,18 @@ def order(key):
     return o, r
 
 
-def boundary(order_, nblk, block_bytes, gpu_budget, cpu_budget, flags=0):
+def boundary(order_, nblk, block_bytes, gpu_budget, cpu_budget, flags=0, ssd_budget=0, with_ssd=False):
+    """-> (prefix, tier_new, m_gpu, m_cpu), plus m_ssd when with_ssd."""
     o = _need(order_, np.uint32)
     nb = _need(nblk, np.uint32)
     P = o.size
     prefix = np.zeros(P, np.uint64)
     tier_new = np.zeros(P, np.uint8)
-    mg, mc = C.c_uint32(0), C.c_uint32(0)
-    lib().orc_boundary(P, _ptr(o), _ptr(nb), block_bytes, gpu_budget, cpu_budget, flags, _ptr(prefix),
-                       _ptr(tier_new), C.byref(mg), C.byref(mc))
+    mg, mc, ms = C.c_uint32(0), C.c_uint32(0), C.c_uint32(0)
+    lib().orc_boundary(P, _ptr(o), _ptr(nb), block_bytes, gpu_budget, cpu_budget, ssd_budget, flags, _ptr(prefix),
+                       _ptr(tier_new), C.byref(mg), C.byref(mc), C.byref(ms))
+    if with_ssd:
+        return prefix, tier_new, mg.value, mc.value, ms.value
     return prefix, tier_new, mg.value, mc.value
 
 
@@ -157,7 +160,7 @@ class Result:
 
 
 def rebalance(geom, *, window=None, iota=None, status=None, tbl_off, tbl, tier, free_map,
-              gpu_budget, cpu_budget, flags=0, pool=None, host_bufs=None, k=None) -> Result:
+              gpu_budget, cpu_budget, flags=0, pool=None, host_bufs=None, k=None, ssd_budget=0) -> Result:
     """One whole rebalance.  ``geom`` has layers, planes, block_tokens, row_bytes, num_blocks.
 
     ``tbl`` (uint32), ``tier`` (uint8), ``free_map`` (uint8), ``pool`` (uint8) and the
@@ -193,7 +196,7 @@ def rebalance(geom, *, window=None, iota=None, status=None, tbl_off, tbl, tier, 
     s = _Summary()
     rc = lib().orc_rebalance(C.byref(g), _ptr(pool), P, kk, _ptr(w), _ptr(it), _ptr(st), _ptr(off),
                              tbl.size, _ptr(tbl), _ptr(tier), _ptr(free_map), int(gpu_budget),
-                             int(cpu_budget), flags, None if bufs is None else C.cast(bufs, C.c_void_p),
+                             int(cpu_budget), int(ssd_budget), flags, None if bufs is None else C.cast(bufs, C.c_void_p),
                              _ptr(order_), _ptr(rank), _ptr(tier_old), _ptr(cat), _ptr(prefix), C.byref(s))
     summary = {name: getattr(s, name) for name, _ in _Summary._fields_} if rc == OK else {}
     return Result(rc, order_, rank, tier_old, cat, prefix, summary)

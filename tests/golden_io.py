@@ -87,3 +87,15 @@ def incremental_cases():
             d[key] = int(kv[key])
         res[name] = d
     return res
+
+
+def ssd_cases():
+    sections, _ = _kv_blocks(os.path.join(GOLDEN, "ssd_worked.txt"))
+    res = {}
+    for name, kv in sections.items():
+        d = {k: [int(x) for x in kv[k].split()] for k in ("blocks", "tier", "new_tier", "category", "m")}
+        d["idleness"] = [float(x) for x in kv["idleness"].split()]
+        for key in ("gpu_budget", "cpu_budget", "ssd_budget", "skip_fit"):
+            d[key] = int(kv[key])
+        res[name] = d
+    return res
