@@ -83,12 +83,14 @@ extern "C" {
 #define MORI_TIER_GPU 0u
 #define MORI_TIER_CPU 1u
 #define MORI_TIER_WAIT 2u
+#define MORI_TIER_SSD 3u /* only with MORI_F_SSD_TIER (Sec. 7.1: storage below the CPU tier) */
 #define MORI_NO_PAGE 0xFFFFFFFFu
 
 #define MORI_F_STATUS_KEY 1u     /* Acting programs (status 1) rank after all Reasoning ones */
 #define MORI_F_SKIP_FIT 2u       /* greedy fit in rank order instead of a strict prefix */
 #define MORI_F_IDLENESS_GIVEN 4u /* use programs.idleness instead of windows */
 #define MORI_F_INCREMENTAL 8u    /* incremental sticky policy of Sec. 4.3.1 instead of the boundary */
+#define MORI_F_SSD_TIER 16u      /* a third boundary in the ranking: the SSD tier (Sec. 7.1) */
 
 /* program status (Sec. 4.1), read with MORI_F_STATUS_KEY or MORI_F_INCREMENTAL */
 #define MORI_ST_REASONING 0u /* running inference or waiting for it */
@@ -101,12 +103,16 @@ extern "C" {
 
 /* transition categories (mori_plan.category) */
 #define MORI_CAT_KEPT 0u
-#define MORI_CAT_OUT 1u       /* GPU -> CPU: bytes gathered to the host */
-#define MORI_CAT_IN 2u        /* CPU -> GPU: bytes scattered into new pages */
+#define MORI_CAT_OUT 1u       /* GPU -> CPU or SSD: bytes gathered to the host */
+#define MORI_CAT_IN 2u        /* CPU or SSD -> GPU: bytes scattered into new pages */
 #define MORI_CAT_DROP_GPU 3u  /* GPU -> Waiting: pages released, KV discarded */
 #define MORI_CAT_DROP_CPU 4u  /* CPU -> Waiting */
 #define MORI_CAT_ADMIT_GPU 5u /* Waiting -> GPU: pages reserved, no copy */
 #define MORI_CAT_ADMIT_CPU 6u /* Waiting -> CPU: no copy */
+#define MORI_CAT_CPU_SSD 7u   /* CPU -> SSD: the caller writes the host buffer to storage */
+#define MORI_CAT_SSD_CPU 8u   /* SSD -> CPU: the caller reads it back into a host buffer */
+#define MORI_CAT_DROP_SSD 9u  /* SSD -> Waiting */
+#define MORI_CAT_ADMIT_SSD 10u /* Waiting -> SSD: no copy */
 
 #define MORI_MAX_PROGRAMS 4096u
 #define MORI_MAX_WINDOW 64u
@@ -146,6 +152,7 @@ typedef struct {
   uint64_t gpu_bytes; /* <= num_blocks * block bytes */
   uint64_t cpu_bytes;
   uint32_t flags;     /* MORI_F_* */
+  uint64_t ssd_bytes; /* read only with MORI_F_SSD_TIER */
 } mori_budget;
 
 /* The plan of the last mori_rank_partition, as mirrored on the host.  The
@@ -155,9 +162,10 @@ typedef struct {
   uint32_t num_programs, m_gpu, m_cpu;
   uint32_t n_out, n_in, n_drop_gpu, n_drop_cpu, n_admit_gpu, n_admit_cpu;
   uint32_t device_error; /* MORI_DEV_* bits; 0 when the plan is valid */
+  uint32_t m_ssd;        /* programs on the SSD tier (0 without MORI_F_SSD_TIER) */
   uint64_t pages_out, pages_in, pages_admit;
   uint64_t pages_free_before, pages_released, pages_recycled, pages_free_after;
-  uint64_t bytes_out, bytes_in, gpu_bytes_after, cpu_bytes_after;
+  uint64_t bytes_out, bytes_in, gpu_bytes_after, cpu_bytes_after, ssd_bytes_after;
   const uint32_t* order;        /* [P] program ids, busiest first (incremental: see below) */
   const uint64_t* prefix;       /* [P] inclusive KV-byte prefix in rank order */
   const uint8_t* tier_old;      /* [P] */
@@ -229,9 +237,18 @@ int mori_host_free(void* ptr);
  * m_cpu count the programs on each tier afterwards.  A new arrival must have
  * fewer than 2^31 blocks (MORI_DEV_BAD_TBL_OFF otherwise).
  *
+ * MORI_F_SSD_TIER (Sec. 7.1, boundary policy only): tier 3 is valid and the
+ * ranking gets a third run -- after the CPU tier's, the longest run within
+ * ssd_bytes goes to the SSD tier (skip-fit: the first of GPU, CPU, SSD with
+ * room).  An SSD program owns no page; its KV is the caller's, in storage.
+ * A program leaving the GPU for the SSD tier is swapped out like one going to
+ * the CPU tier (into a host buffer the caller then writes to storage), and one
+ * coming back is swapped in from a host buffer the caller has filled; page
+ * slots go to every swapped-in program (from CPU or SSD) in rank order.
+ *
  * EINVAL: null pointers (status with MORI_F_STATUS_KEY or MORI_F_INCREMENTAL),
- * P > max_programs, window_k out of range, unknown flags, gpu_bytes >
- * num_blocks * block bytes. */
+ * P > max_programs, window_k out of range, unknown flags, MORI_F_SSD_TIER with
+ * MORI_F_INCREMENTAL, gpu_bytes > num_blocks * block bytes. */
 int mori_rank_partition(mori_ctx* ctx, const mori_programs* programs, const mori_budget* budget,
                         void* stream);
 

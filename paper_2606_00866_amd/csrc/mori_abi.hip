@@ -301,8 +301,10 @@ extern "C" int mori_rank_partition(mori_ctx* ctx, const mori_programs* pr, const
   if (!ctx || !pr || !b) return MORI_EINVAL;
   const uint32_t P = pr->num_programs;
   if (P > ctx->max_programs) return MORI_ENOSPC;
-  if (b->flags & ~(MORI_F_STATUS_KEY | MORI_F_SKIP_FIT | MORI_F_IDLENESS_GIVEN | MORI_F_INCREMENTAL))
+  if (b->flags & ~(MORI_F_STATUS_KEY | MORI_F_SKIP_FIT | MORI_F_IDLENESS_GIVEN | MORI_F_INCREMENTAL |
+                   MORI_F_SSD_TIER))
     return MORI_EINVAL;
+  if ((b->flags & MORI_F_SSD_TIER) && (b->flags & MORI_F_INCREMENTAL)) return MORI_EINVAL;
   if (!pr->tbl_off || !pr->free_map) return MORI_EINVAL;
   if (P && (!pr->tier || (pr->tbl_len && !pr->tbl))) return MORI_EINVAL;
   if (b->flags & MORI_F_IDLENESS_GIVEN) {
@@ -335,6 +337,7 @@ extern "C" int mori_rank_partition(mori_ctx* ctx, const mori_programs* pr, const
   a.block_bytes = ctx->block_bytes;
   a.gpu_bytes = b->gpu_bytes;
   a.cpu_bytes = b->cpu_bytes;
+  a.ssd_bytes = (b->flags & MORI_F_SSD_TIER) ? b->ssd_bytes : 0;
   a.sum = ctx->sum_dev();
   a.order = ctx->dev<uint32_t>(ctx->L.order);
   a.prefix = ctx->dev<uint64_t>(ctx->L.prefix);
@@ -390,6 +393,8 @@ extern "C" int mori_plan_wait(mori_ctx* ctx, mori_plan* out) {
   p.bytes_in = s->bytes_in;
   p.gpu_bytes_after = s->gpu_bytes_after;
   p.cpu_bytes_after = s->cpu_bytes_after;
+  p.ssd_bytes_after = s->ssd_bytes_after;
+  p.m_ssd = s->m_ssd;
   p.order = ctx->host<uint32_t>(ctx->L.order);
   p.prefix = ctx->host<uint64_t>(ctx->L.prefix);
   p.tier_old = ctx->host<uint8_t>(ctx->L.tier_old);

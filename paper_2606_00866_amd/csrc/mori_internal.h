@@ -18,12 +18,12 @@ constexpr int PAGE_WG = 256;       // threads per page-allocation workgroup (16 
 
 // Plan summary as kept on the device (the head of the plan blob copied to the host).
 struct DevSummary {
-  uint32_t num_programs, m_gpu, m_cpu;
+  uint32_t num_programs, m_gpu, m_cpu, m_ssd;
   uint32_t n_out, n_in, n_drop_gpu, n_drop_cpu, n_admit_gpu, n_admit_cpu;
   uint32_t error;
   uint64_t pages_out, pages_in, pages_admit;
   uint64_t pages_free_before, pages_released, pages_recycled, pages_free_after;
-  uint64_t bytes_out, bytes_in, gpu_bytes_after, cpu_bytes_after;
+  uint64_t bytes_out, bytes_in, gpu_bytes_after, cpu_bytes_after, ssd_bytes_after;
   uint64_t need;  // pages_in + pages_admit
 };
 
@@ -46,7 +46,7 @@ struct PlanArgs {
   uint8_t* tier;
   uint8_t* free_map;
   uint32_t tbl_len, P, k, flags, NB, ntiles;
-  uint64_t block_bytes, gpu_bytes, cpu_bytes;
+  uint64_t block_bytes, gpu_bytes, cpu_bytes, ssd_bytes;
   // context scratch: plan blob (mirrored to the host)
   DevSummary* sum;
   uint32_t* order;

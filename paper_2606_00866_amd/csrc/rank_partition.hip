@@ -68,11 +68,19 @@ __device__ T block_scan_excl(T v, T* s_wave, T* total) {
   return res;
 }
 
+// Transition category.  Leaving the GPU for a tier that keeps the KV (CPU,
+// SSD) is a swap-out, the reverse a swap-in.
 __device__ inline uint8_t category(uint8_t from, uint8_t to) {
   if (from == to) return MORI_CAT_KEPT;
-  if (from == MORI_TIER_GPU) return to == MORI_TIER_CPU ? MORI_CAT_OUT : MORI_CAT_DROP_GPU;
-  if (from == MORI_TIER_CPU) return to == MORI_TIER_GPU ? MORI_CAT_IN : MORI_CAT_DROP_CPU;
-  return to == MORI_TIER_GPU ? MORI_CAT_ADMIT_GPU : MORI_CAT_ADMIT_CPU;
+  switch (from) {
+    case MORI_TIER_GPU: return to == MORI_TIER_WAIT ? MORI_CAT_DROP_GPU : MORI_CAT_OUT;
+    case MORI_TIER_CPU:
+      return to == MORI_TIER_GPU ? MORI_CAT_IN : (to == MORI_TIER_SSD ? MORI_CAT_CPU_SSD : MORI_CAT_DROP_CPU);
+    case MORI_TIER_SSD:
+      return to == MORI_TIER_GPU ? MORI_CAT_IN : (to == MORI_TIER_CPU ? MORI_CAT_SSD_CPU : MORI_CAT_DROP_SSD);
+    default:
+      return to == MORI_TIER_GPU ? MORI_CAT_ADMIT_GPU : (to == MORI_TIER_CPU ? MORI_CAT_ADMIT_CPU : MORI_CAT_ADMIT_SSD);
+  }
 }
 
 __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
@@ -83,24 +91,26 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
   __shared__ uint64_t s_w64[NW + 1];
   __shared__ uint32_t s_w32[NW + 1];
   __shared__ unsigned long long s_or, s_and;
-  __shared__ uint32_t s_err, s_m_gpu, s_m_cpu;
+  __shared__ uint32_t s_err, s_m_gpu, s_m_cpu, s_m_ssd;
   __shared__ uint32_t s_grp[5], s_cpu_reasoning, s_k_gpu, s_k_cpu;
   __shared__ uint32_t s_n_drop_gpu, s_n_drop_cpu, s_n_admit_gpu, s_n_admit_cpu;
-  __shared__ unsigned long long s_gpu_after, s_cpu_after, s_gpu_part;
+  __shared__ unsigned long long s_gpu_after, s_cpu_after, s_ssd_after, s_gpu_part, s_upper_part;
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const uint32_t P = a.P;
   const bool incremental = (a.flags & MORI_F_INCREMENTAL) != 0;
+  const bool ssd = (a.flags & MORI_F_SSD_TIER) != 0;
+  const uint8_t top_tier = ssd ? MORI_TIER_SSD : MORI_TIER_WAIT;
   if (tid == 0) {
     s_err = 0;
     s_or = 0;
     s_and = ~0ull;
-    s_m_gpu = s_m_cpu = 0;
+    s_m_gpu = s_m_cpu = s_m_ssd = 0;
     for (int g = 0; g < 5; ++g) s_grp[g] = 0;
     s_cpu_reasoning = s_k_gpu = s_k_cpu = 0;
     s_n_drop_gpu = s_n_drop_cpu = s_n_admit_gpu = s_n_admit_cpu = 0;
-    s_gpu_after = s_cpu_after = 0;
-    s_gpu_part = 0;
+    s_gpu_after = s_cpu_after = s_ssd_after = 0;
+    s_gpu_part = s_upper_part = 0;
     DevSummary z = {};
     z.num_programs = P;
     *a.sum = z;
@@ -125,7 +135,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     if (x >= P) continue;
     const uint8_t told = a.tier[x];
     const uint32_t off0 = a.tbl_off[x], off1 = a.tbl_off[x + 1];
-    if (told > MORI_TIER_WAIT) err |= MORI_DEV_BAD_TIER;
+    if (told > top_tier) err |= MORI_DEV_BAD_TIER;
     if (off1 < off0) err |= MORI_DEV_BAD_TBL_OFF;
     float v;
     if (a.flags & MORI_F_IDLENESS_GIVEN) {
@@ -375,18 +385,37 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     }
     if (c) atomicAdd(&s_m_cpu, c);
     __syncthreads();
-    const uint32_t m_cpu = s_m_cpu;
+    const uint32_t m_cpu = s_m_cpu, upper = m_gpu + m_cpu;
+    uint32_t m_ssd = 0;
+    if (ssd) {  // Sec. 7.1: the run after the CPU tier's, within the SSD budget
+#pragma unroll
+      for (int it = 0; it < IPT; ++it)
+        if (upper > 0 && it * RT + tid == (int)upper - 1) s_upper_part = S[it];
+      __syncthreads();
+      const uint64_t upper_part = s_upper_part;
+      c = 0;
+#pragma unroll
+      for (int it = 0; it < IPT; ++it) {
+        const uint32_t r = it * RT + tid;
+        if (r >= upper && r < P && S[it] - upper_part <= a.ssd_bytes) ++c;
+      }
+      if (c) atomicAdd(&s_m_ssd, c);
+      __syncthreads();
+      m_ssd = s_m_ssd;
+    }
 #pragma unroll
     for (int it = 0; it < IPT; ++it) {
       const uint32_t r = it * RT + tid;
-      s_tier[r] = r < m_gpu ? MORI_TIER_GPU : (r < m_gpu + m_cpu ? MORI_TIER_CPU : MORI_TIER_WAIT);
+      s_tier[r] = r < m_gpu ? MORI_TIER_GPU
+                : r < upper ? MORI_TIER_CPU
+                : r < upper + m_ssd ? MORI_TIER_SSD : MORI_TIER_WAIT;
     }
   } else {
     // Greedy walk in rank order: first tier that still has room.
     __syncthreads();
     if (tid == 0) {
-      uint64_t room_gpu = a.gpu_bytes, room_cpu = a.cpu_bytes;
-      uint32_t ng = 0, nc = 0;
+      uint64_t room_gpu = a.gpu_bytes, room_cpu = a.cpu_bytes, room_ssd = a.ssd_bytes;
+      uint32_t ng = 0, nc = 0, ns = 0;
       for (uint32_t r = 0; r < P; ++r) {
         const uint64_t bytes = (uint64_t)s_id[r] * a.block_bytes;
         if (bytes <= room_gpu) {
@@ -397,12 +426,17 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
           room_cpu -= bytes;
           s_tier[r] = MORI_TIER_CPU;
           ++nc;
+        } else if (ssd && bytes <= room_ssd) {
+          room_ssd -= bytes;
+          s_tier[r] = MORI_TIER_SSD;
+          ++ns;
         } else {
           s_tier[r] = MORI_TIER_WAIT;
         }
       }
       s_m_gpu = ng;
       s_m_cpu = nc;
+      s_m_ssd = ns;
     }
   }
   __syncthreads();
@@ -413,7 +447,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
   uint8_t catv[IPT];
   uint64_t carryA = 0, carryB = 0;
   uint32_t n_dg = 0, n_dc = 0, n_ag = 0, n_ac = 0;
-  uint64_t gpu_after = 0, cpu_after = 0;
+  uint64_t gpu_after = 0, cpu_after = 0, ssd_after = 0;
 #pragma unroll
   for (int it = 0; it < IPT; ++it) {
     const uint32_t r = it * RT + tid;
@@ -435,6 +469,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
       if (c == MORI_CAT_ADMIT_CPU) ++n_ac;
       if (tnew == MORI_TIER_GPU) gpu_after += (uint64_t)nb[it] * a.block_bytes;
       if (tnew == MORI_TIER_CPU) cpu_after += (uint64_t)nb[it] * a.block_bytes;
+      if (tnew == MORI_TIER_SSD) ssd_after += (uint64_t)nb[it] * a.block_bytes;
     }
     uint64_t tA, tB;
     exA[it] = carryA + block_scan_excl<uint64_t>(va, s_w64, &tA);
@@ -459,7 +494,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
         a.out_pg_base[idx_out] = pg_out_ex;
         a.base[p] = pg_out_ex;
         break;
-      case MORI_CAT_IN:  // promoted CPU programs take the first slots (priority (1) of Sec. 4.3.1)
+      case MORI_CAT_IN:  // programs promoted from the CPU (or SSD) tier take the first slots (Sec. 4.3.1)
         a.in_prog[idx_in] = p;
         a.in_pg_base[idx_in] = pg_in_ex;
         a.base[p] = pg_in_ex;
@@ -477,6 +512,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
   if (n_ac) atomicAdd(&s_n_admit_cpu, n_ac);
   if (gpu_after) atomicAdd(&s_gpu_after, (unsigned long long)gpu_after);
   if (cpu_after) atomicAdd(&s_cpu_after, (unsigned long long)cpu_after);
+  if (ssd_after) atomicAdd(&s_ssd_after, (unsigned long long)ssd_after);
   __syncthreads();
   if (tid == 0) {
     a.out_pg_base[n_out] = pages_out;
@@ -484,6 +520,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     DevSummary* s = a.sum;
     s->m_gpu = s_m_gpu;
     s->m_cpu = s_m_cpu;
+    s->m_ssd = s_m_ssd;
     s->n_out = n_out;
     s->n_in = n_in;
     s->n_drop_gpu = s_n_drop_gpu;
@@ -497,6 +534,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     s->bytes_in = (uint64_t)pages_in * a.block_bytes;
     s->gpu_bytes_after = s_gpu_after;
     s->cpu_bytes_after = s_cpu_after;
+    s->ssd_bytes_after = s_ssd_after;
     s->need = (uint64_t)pages_in + pages_admit;
   }
 }

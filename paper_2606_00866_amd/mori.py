@@ -18,13 +18,13 @@ MORI_DEV_BAD_WINDOW, MORI_DEV_BAD_IDLENESS, MORI_DEV_BAD_TIER, MORI_DEV_BAD_TBL_
 MORI_DEV_PAGE_RANGE, MORI_DEV_PAGE_DUP, MORI_DEV_PAGE_LEAK, MORI_DEV_NONRES_PAGE = 0x10, 0x20, 0x40, 0x80
 MORI_DEV_NOSPC, MORI_DEV_HOST_ADDR, MORI_DEV_BAD_BLOCK, MORI_DEV_BAD_STATUS = 0x100, 0x200, 0x400, 0x800
 MORI_TYPE_BUSY, MORI_TYPE_IDLE, MORI_TYPE_INACTIVE = 0, 1, 2
-MORI_TIER_GPU, MORI_TIER_CPU, MORI_TIER_WAIT = 0, 1, 2
+MORI_TIER_GPU, MORI_TIER_CPU, MORI_TIER_WAIT, MORI_TIER_SSD = 0, 1, 2, 3
 MORI_NO_PAGE = 0xFFFFFFFF
-MORI_F_STATUS_KEY, MORI_F_SKIP_FIT, MORI_F_IDLENESS_GIVEN, MORI_F_INCREMENTAL = 1, 2, 4, 8
+MORI_F_STATUS_KEY, MORI_F_SKIP_FIT, MORI_F_IDLENESS_GIVEN, MORI_F_INCREMENTAL, MORI_F_SSD_TIER = 1, 2, 4, 8, 16
 MORI_ST_REASONING, MORI_ST_ACTING, MORI_ST_NEW = 0, 1, 2
 MORI_COPY_AUTO, MORI_COPY_KERNEL, MORI_COPY_CE = 0, 1, 2
 (MORI_CAT_KEPT, MORI_CAT_OUT, MORI_CAT_IN, MORI_CAT_DROP_GPU, MORI_CAT_DROP_CPU, MORI_CAT_ADMIT_GPU,
- MORI_CAT_ADMIT_CPU) = range(7)
+ MORI_CAT_ADMIT_CPU, MORI_CAT_CPU_SSD, MORI_CAT_SSD_CPU, MORI_CAT_DROP_SSD, MORI_CAT_ADMIT_SSD) = range(11)
 MORI_MAX_PROGRAMS, MORI_MAX_WINDOW, MORI_MAX_RANGES = 4096, 64, 64
 MORI_Q_LAST_HIP_ERROR, MORI_Q_DEVICE_ERROR, MORI_Q_LAST_MODE = 1, 2, 3
 MORI_Q_PLAN_EVENT, MORI_Q_OUT_EVENT, MORI_Q_IN_EVENT = 4, 5, 6
@@ -46,7 +46,8 @@ class mori_programs(C.Structure):
 
 
 class mori_budget(C.Structure):
-    _fields_ = [("gpu_bytes", C.c_uint64), ("cpu_bytes", C.c_uint64), ("flags", C.c_uint32)]
+    _fields_ = [("gpu_bytes", C.c_uint64), ("cpu_bytes", C.c_uint64), ("flags", C.c_uint32),
+                ("ssd_bytes", C.c_uint64)]
 
 
 class mori_blocks(C.Structure):
@@ -57,9 +58,9 @@ class mori_blocks(C.Structure):
 class mori_plan(C.Structure):
     _fields_ = [(n, C.c_uint32) for n in (
         "num_programs", "m_gpu", "m_cpu", "n_out", "n_in", "n_drop_gpu", "n_drop_cpu", "n_admit_gpu",
-        "n_admit_cpu", "device_error")] + [(n, C.c_uint64) for n in (
+        "n_admit_cpu", "device_error", "m_ssd")] + [(n, C.c_uint64) for n in (
             "pages_out", "pages_in", "pages_admit", "pages_free_before", "pages_released", "pages_recycled",
-            "pages_free_after", "bytes_out", "bytes_in", "gpu_bytes_after", "cpu_bytes_after")] + [
+            "pages_free_after", "bytes_out", "bytes_in", "gpu_bytes_after", "cpu_bytes_after", "ssd_bytes_after")] + [
         ("order", C.POINTER(C.c_uint32)), ("prefix", C.POINTER(C.c_uint64)), ("tier_old", C.POINTER(C.c_uint8)),
         ("tier_new", C.POINTER(C.c_uint8)), ("category", C.POINTER(C.c_uint8)),
         ("out_programs", C.POINTER(C.c_uint32)), ("in_programs", C.POINTER(C.c_uint32))]

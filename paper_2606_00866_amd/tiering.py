@@ -163,14 +163,14 @@ class TierPool:
     # ---- the three calls -----------------------------------------------------
     def rank_partition(self, *, gpu_bytes: int, cpu_bytes: int, window: torch.Tensor | None = None,
                        idleness: torch.Tensor | None = None, status: torch.Tensor | None = None, flags: int = 0,
-                       stream: torch.cuda.Stream | None = None) -> int:
+                       stream: torch.cuda.Stream | None = None, ssd_bytes: int = 0) -> int:
         k = int(window.shape[1]) if window is not None else 0
         prog = M.mori_programs(self.P, k, window.data_ptr() if window is not None else None,
                                idleness.data_ptr() if idleness is not None else None,
                                status.data_ptr() if status is not None else None, self.tbl_off.data_ptr(),
                                self.tbl_len, self.tbl.data_ptr(), self.tier.data_ptr(), self.free_map.data_ptr())
         self._keep = [window, idleness, status]
-        budget = M.mori_budget(int(gpu_bytes), int(cpu_bytes), int(flags))
+        budget = M.mori_budget(int(gpu_bytes), int(cpu_bytes), int(flags), int(ssd_bytes))
         return M.mori_rank_partition(self.ctx, prog, budget, _stream(stream))
 
     def plan_wait(self):
@@ -189,12 +189,14 @@ class TierPool:
 
     def place_host_buffers(self) -> None:
         """Caller's host-extent bookkeeping for the current plan: drop the
-        buffers of CPU programs sent to Waiting, give buffers to programs that
-        enter the CPU tier (those moving out, and those admitted from Waiting)."""
+        buffers of CPU (or SSD) programs sent to Waiting, give buffers to
+        programs that leave the GPU and to those admitted from Waiting to the
+        CPU (or SSD) tier.  An SSD program's KV is kept in its host buffer here:
+        the storage I/O of the SSD tier is outside this module."""
         cat = self.plan_arrays()["category"]
-        for p in np.flatnonzero(cat == M.MORI_CAT_DROP_CPU):
+        for p in np.flatnonzero((cat == M.MORI_CAT_DROP_CPU) | (cat == M.MORI_CAT_DROP_SSD)):
             self.drop_host_buffer(int(p))
-        for c in (M.MORI_CAT_OUT, M.MORI_CAT_ADMIT_CPU):
+        for c in (M.MORI_CAT_OUT, M.MORI_CAT_ADMIT_CPU, M.MORI_CAT_ADMIT_SSD):
             for p in np.flatnonzero(cat == c):
                 self.give_host_buffer(int(p))
 
@@ -211,10 +213,11 @@ class TierPool:
             self.drop_host_buffer(int(p))
 
     def step(self, *, gpu_bytes: int, cpu_bytes: int, window=None, idleness=None, status=None, flags: int = 0,
-             mode: int = M.MORI_COPY_AUTO, s_out=None, s_in=None, sync: bool = True):
+             mode: int = M.MORI_COPY_AUTO, s_out=None, s_in=None, sync: bool = True, ssd_bytes: int = 0):
         """rank -> plan on the host -> host extents -> swap-out || swap-in."""
         check(self.rank_partition(gpu_bytes=gpu_bytes, cpu_bytes=cpu_bytes, window=window, idleness=idleness,
-                                  status=status, flags=flags, stream=s_out), "mori_rank_partition")
+                                  status=status, flags=flags, stream=s_out, ssd_bytes=ssd_bytes),
+              "mori_rank_partition")
         rc, p = self.plan_wait()
         if rc != M.MORI_OK:
             raise MoriError("mori_plan_wait", rc, p.device_error)

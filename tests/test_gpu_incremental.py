@@ -9,7 +9,7 @@ import pytest
 import torch
 
 from golden_io import incremental_cases
-from gpu_helpers import Pair, log
+from gpu_helpers import Pair, instance_from_blocks, log
 from oracle import oracle
 from paper_2606_00866_amd import mori as M
 from workload import Geometry, random_instance
@@ -26,36 +26,10 @@ def _lib():
     M.lib()
 
 
-def _instance_from_case(c, extra_free=3, seed=0):
-    """A consistent pool holding the fixture's programs (one block = 16 bytes)."""
-    P = len(c["blocks"])
-    rng = np.random.default_rng(seed)
-    inst = random_instance(rng, P=P, geom=Geometry(1, 1, 1, 16, 0), extra_free=0)
-    nblk = np.array(c["blocks"], np.uint32)
-    tier = np.array(c["tier"], np.uint8)
-    NB = max(int(nblk[tier == 0].sum()) + extra_free, c["gpu_budget"])  # the budget fits the pool
-    geom = Geometry(1, 1, 1, 16, NB)
-    off = np.zeros(P + 1, np.uint32)
-    off[1:] = np.cumsum(nblk)
-    tbl = np.full(int(off[-1]), M.MORI_NO_PAGE, np.uint32)
-    perm = rng.permutation(NB).astype(np.uint32)
-    used = 0
-    for p in range(P):
-        if tier[p] == 0:
-            tbl[off[p]:off[p + 1]] = perm[used:used + nblk[p]]
-            used += int(nblk[p])
-    free = np.zeros(NB, np.uint8)
-    free[perm[used:]] = 1
-    inst.geom, inst.nblk, inst.tbl_off, inst.tbl, inst.tier, inst.free_map = geom, nblk, off, tbl, tier, free
-    inst.ctx = nblk.astype(np.int64)
-    inst.status = np.array(c["status"], np.uint8)
-    return inst
-
-
 @pytest.mark.parametrize("name", sorted(incremental_cases()))
 def test_worked_examples(name):
     c = incremental_cases()[name]
-    inst = _instance_from_case(c)
+    inst = instance_from_blocks(c["blocks"], c["tier"], c["gpu_budget"], status=c["status"])
     flags = INC | M.MORI_F_IDLENESS_GIVEN | (M.MORI_F_SKIP_FIT if c["skip_fit"] else 0)
     log(f"incremental worked example {name}")
     pair = Pair(inst, seed=11)

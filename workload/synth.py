@@ -207,7 +207,7 @@ def random_instance(rng, P: int | None = None, max_blocks: int = 12, geom: Geome
         geom = Geometry(int(rng.integers(1, 4)), int(rng.integers(1, 3)), int(rng.choice([1, 2, 4, 16])),
                         int(rng.choice([16, 32, 48, 512, 1152])), 0)
     nblk = rng.integers(0, max_blocks + 1, size=P).astype(np.uint32)
-    tier = rng.choice(3, size=P, p=list(tier_p)).astype(np.uint8)
+    tier = rng.choice(len(tier_p), size=P, p=list(tier_p)).astype(np.uint8)  # a 4th entry: SSD tier (3)
     gpu_blocks = int(nblk[tier == TIER_GPU].astype(np.int64).sum())
     if extra_free is None:
         extra_free = int(rng.integers(0, 2 * max_blocks + 1))
