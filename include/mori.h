@@ -334,6 +334,33 @@ int mori_profile(mori_ctx* ctx, int enable);
 int mori_profile_read(mori_ctx* ctx, int direction, uint64_t* launches, uint64_t* payload_bytes,
                       double* kernel_ms);
 
+/* ---- multi-replica admission (host) ----------------------------------- */
+#define MORI_MAX_REPLICAS 1024u
+#define MORI_ADMIT_BEST_FIT 1u /* least room that holds the program, instead of the most */
+
+/* Admission of the Waiting queue that all replicas share (Sec. 4.1: a GPU and
+ * a CPU queue per replica, one global Waiting queue; Sec. 4.3.1: Waiting
+ * promotions are bin-packed across replicas in decreasing size onto the
+ * replica with the most available capacity, while CPU-tier programs keep their
+ * replica -- each replica's own mori_rank_partition promotes those).  Host
+ * memory only; no GPU work.
+ *   bytes[P], idleness[P], status[P]: the Waiting programs' KV bytes, Eq. 1
+ *     idleness in [0, 1] and MORI_ST_* status.  Candidates are the Reasoning
+ *     (returning) programs, then the new arrivals; Acting programs stay.
+ *     Within a level: larger KV first, then lower idleness, then lower index.
+ *   room[R]: free GPU bytes of each replica after its own plan.
+ *   flags: 0 or MORI_ADMIT_BEST_FIT.
+ *   replica[P] (out): the replica each program goes to, -1 if it stays
+ *     waiting (it fits no replica when its turn comes; later ones are tried).
+ *   room_after[R] (out; may be room itself): room less what was admitted.
+ * Ties between replicas go to the lower index.  Each replica then admits its
+ * programs as Waiting->GPU in its next plan (prefill rebuilds their KV).
+ * EINVAL: num_replicas 0 or above MORI_MAX_REPLICAS, null arrays, unknown
+ * flags, a status above 2 or idleness outside [0, 1]. */
+int mori_replica_admit(uint32_t num_programs, const uint64_t* bytes, const float* idleness, const uint8_t* status,
+                       uint32_t num_replicas, const uint64_t* room, uint32_t flags, int32_t* replica,
+                       uint64_t* room_after);
+
 #ifdef __cplusplus
 }
 #endif

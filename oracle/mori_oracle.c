@@ -587,3 +587,56 @@ int orc_evict_order(uint32_t N, const uint8_t* type, const uint64_t* last_access
   free(v);
   return ORC_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Multi-replica admission (Sec. 4.1 global Waiting queue; Sec. 4.3.1,        */
+/* promotion to GPU, multi-replica deployments).                             */
+/* Reading: the paper names Best-Fit-Decreasing but selects the replica with  */
+/* the most available capacity; that stated selection is the default, the   */
+/* textbook best fit (least sufficient room) is ORC_ADMIT_BEST_FIT.  The     */
+/* single-replica level order is kept (returning before new) and each level  */
+/* is taken in decreasing size, the "decreasing" of the packing.             */
+/* ------------------------------------------------------------------------ */
+/* nonzero when candidate x is packed before candidate y */
+static int orc_pack_before(const uint64_t* bytes, const float* iota, const uint8_t* status, uint32_t x, uint32_t y) {
+  uint32_t lx = status[x] == ORC_ST_NEW, ly = status[y] == ORC_ST_NEW;
+  if (lx != ly) return lx < ly;
+  if (bytes[x] != bytes[y]) return bytes[x] > bytes[y];
+  if (iota[x] != iota[y]) return iota[x] < iota[y];
+  return x < y;
+}
+
+int orc_replica_admit(uint32_t P, const uint64_t* bytes, const float* iota, const uint8_t* status, uint32_t R,
+                      const uint64_t* room, uint32_t flags, int32_t* replica, uint64_t* room_after) {
+  if (R == 0) return ORC_E_INPUT;
+  for (uint32_t p = 0; p < P; ++p)
+    if (status[p] > ORC_ST_NEW || !(iota[p] >= 0.0f && iota[p] <= 1.0f)) return ORC_E_INPUT;
+  for (uint32_t r = 0; r < R; ++r) room_after[r] = room[r];
+  uint8_t* done = (uint8_t*)calloc(P ? P : 1, 1);
+  for (uint32_t p = 0; p < P; ++p) {
+    replica[p] = -1;
+    if (status[p] == ORC_ST_ACTING) done[p] = 1; /* in a tool call: no inference to admit */
+  }
+  for (;;) {
+    /* the next candidate in packing order */
+    uint32_t c = P;
+    for (uint32_t p = 0; p < P; ++p)
+      if (!done[p] && (c == P || orc_pack_before(bytes, iota, status, p, c))) c = p;
+    if (c == P) break;
+    done[c] = 1;
+    /* the replica it goes to */
+    uint32_t best = R;
+    for (uint32_t r = 0; r < R; ++r) {
+      if (room_after[r] < bytes[c]) continue;
+      if (best == R) best = r;
+      else if (!(flags & ORC_ADMIT_BEST_FIT) && room_after[r] > room_after[best]) best = r;
+      else if ((flags & ORC_ADMIT_BEST_FIT) && room_after[r] < room_after[best]) best = r;
+    }
+    if (best < R) {
+      replica[c] = (int32_t)best;
+      room_after[best] -= bytes[c];
+    }
+  }
+  free(done);
+  return ORC_OK;
+}

@@ -172,6 +172,25 @@ int orc_evict_order(uint32_t N, const uint8_t* type, const uint64_t* last_access
                     uint64_t unit_bytes, uint32_t tier, uint64_t need_bytes, uint32_t* order, uint64_t* prefix,
                     uint32_t* count);
 
+/* ------------------------------------------------------------------------ */
+/* Multi-replica admission of the shared Waiting queue (Sec. 4.1: one global */
+/* Waiting queue, a GPU and a CPU queue per replica; Sec. 4.3.1: Waiting     */
+/* promotions are bin-packed across replicas in decreasing size order, onto  */
+/* the replica with the most available capacity; CPU-tier programs keep     */
+/* their replica and are promoted there).                                     */
+/* Candidates: status Reasoning (returning) before New; Acting programs stay */
+/* waiting.  Within a level: larger KV first, then lower idleness, then id.  */
+/* Each goes to the replica with the most room that can hold it (with        */
+/* ORC_ADMIT_BEST_FIT: the least room that can), ties to the lower replica   */
+/* index; if none can, it stays waiting (-1) and the next is tried.          */
+/* ------------------------------------------------------------------------ */
+#define ORC_ADMIT_BEST_FIT 1u
+
+/* replica[p] in [0, R) or -1; room_after[R] = room minus what was admitted.
+ * ORC_E_INPUT for R == 0, a status above 2 or idleness outside [0, 1]. */
+int orc_replica_admit(uint32_t P, const uint64_t* bytes, const float* iota, const uint8_t* status, uint32_t R,
+                      const uint64_t* room, uint32_t flags, int32_t* replica, uint64_t* room_after);
+
 #ifdef __cplusplus
 }
 #endif

@@ -27,6 +27,7 @@ NONE = 0xFFFFFFFF
 F_STATUS_KEY, F_SKIP_FIT, F_IDLENESS_GIVEN, F_INCREMENTAL, F_SSD_TIER = 1, 2, 4, 8, 16
 ST_REASONING, ST_ACTING, ST_NEW = 0, 1, 2
 OK, E_INPUT, E_POOL, E_NOSPC = 0, 1, 2, 3
+ADMIT_BEST_FIT = 1
 KEPT, OUT, IN, DROP_GPU, DROP_CPU, ADMIT_GPU, ADMIT_CPU, CPU_SSD, SSD_CPU, DROP_SSD, ADMIT_SSD = range(11)
 
 
@@ -76,6 +77,7 @@ def lib():
                                        C.c_uint64, C.c_uint64, C.c_uint64, C.c_uint32, P, P, P, P, P, P, P]
         _lib.orc_incremental.argtypes = [C.c_uint32, P, P, P, P, C.c_uint64, C.c_uint64, C.c_uint64, C.c_uint32,
                                          P, P, P, P, P, P]
+        _lib.orc_replica_admit.argtypes = [C.c_uint32, P, P, P, C.c_uint32, P, C.c_uint32, P, P]
         _lib.orc_evict_order.argtypes = [C.c_uint32, P, P, P, C.c_uint64, C.c_uint32, C.c_uint64, P, P, P]
     return _lib
 
@@ -214,3 +216,16 @@ def evict_order(type_, last_access, tier, need_bytes, size=None, unit_bytes=1):
     rc = lib().orc_evict_order(N, _ptr(t), _ptr(la), _ptr(sz), int(unit_bytes), int(tier), int(need_bytes),
                                _ptr(order_), _ptr(prefix), C.byref(cnt))
     return rc, order_, prefix, cnt.value
+
+
+def replica_admit(bytes_, iota, status, room, flags=0):
+    """Multi-replica admission of Waiting programs -> (rc, replica [P] int32, room_after [R])."""
+    b = _need(bytes_, np.uint64)
+    P = b.size
+    it = _need(iota, np.float32, P)
+    st = _need(status, np.uint8, P)
+    rm = _need(room, np.uint64)
+    rep = np.zeros(P, np.int32)
+    after = np.zeros(rm.size, np.uint64)
+    rc = lib().orc_replica_admit(P, _ptr(b), _ptr(it), _ptr(st), rm.size, _ptr(rm), flags, _ptr(rep), _ptr(after))
+    return rc, rep, after

@@ -25,13 +25,15 @@ MORI_ST_REASONING, MORI_ST_ACTING, MORI_ST_NEW = 0, 1, 2
 MORI_COPY_AUTO, MORI_COPY_KERNEL, MORI_COPY_CE = 0, 1, 2
 (MORI_CAT_KEPT, MORI_CAT_OUT, MORI_CAT_IN, MORI_CAT_DROP_GPU, MORI_CAT_DROP_CPU, MORI_CAT_ADMIT_GPU,
  MORI_CAT_ADMIT_CPU, MORI_CAT_CPU_SSD, MORI_CAT_SSD_CPU, MORI_CAT_DROP_SSD, MORI_CAT_ADMIT_SSD) = range(11)
-MORI_MAX_PROGRAMS, MORI_MAX_WINDOW, MORI_MAX_RANGES = 4096, 64, 64
+MORI_MAX_PROGRAMS, MORI_MAX_WINDOW, MORI_MAX_RANGES, MORI_MAX_REPLICAS = 4096, 64, 64, 1024
+MORI_ADMIT_BEST_FIT = 1
 MORI_Q_LAST_HIP_ERROR, MORI_Q_DEVICE_ERROR, MORI_Q_LAST_MODE = 1, 2, 3
 MORI_Q_PLAN_EVENT, MORI_Q_OUT_EVENT, MORI_Q_IN_EVENT = 4, 5, 6
 
 EXPORTS = ("mori_create", "mori_destroy", "mori_register", "mori_host_alloc", "mori_host_free",
            "mori_rank_partition", "mori_plan_wait", "mori_kv_swap_out", "mori_kv_swap_in", "mori_query",
-           "mori_strerror", "mori_profile", "mori_profile_read", "mori_evict_workspace", "mori_evict_order")
+           "mori_strerror", "mori_profile", "mori_profile_read", "mori_evict_workspace", "mori_evict_order",
+           "mori_replica_admit")
 
 
 class mori_pool(C.Structure):
@@ -92,6 +94,7 @@ def lib():
         L.mori_profile_read.argtypes = [V, I, C.POINTER(U64), C.POINTER(U64), C.POINTER(C.c_double)]
         L.mori_evict_workspace.argtypes = [U32, C.POINTER(U64)]
         L.mori_evict_order.argtypes = [C.POINTER(mori_blocks), U32, U64, V, U64, V, V, V, V]
+        L.mori_replica_admit.argtypes = [U32, V, V, V, U32, V, U32, V, V]
         L.mori_strerror.restype = C.c_char_p
         for name in EXPORTS:
             if name != "mori_strerror":
@@ -175,3 +178,20 @@ def mori_evict_order(blocks: mori_blocks, tier: int, need_bytes: int, workspace:
     """order / prefix / result / workspace: device addresses (prefix may be 0)."""
     return lib().mori_evict_order(C.byref(blocks), tier, need_bytes, workspace, workspace_bytes, order,
                                   prefix or None, result, stream)
+
+
+def mori_replica_admit(bytes_, idleness, status, room, flags: int = 0):
+    """Host arrays (numpy) -> (code, replica int32 [P], room_after uint64 [R])."""
+    import numpy as np
+
+    b = np.ascontiguousarray(bytes_, np.uint64)
+    it = np.ascontiguousarray(idleness, np.float32)
+    st = np.ascontiguousarray(status, np.uint8)
+    rm = np.ascontiguousarray(room, np.uint64)
+    assert it.size == b.size and st.size == b.size
+    rep = np.zeros(max(b.size, 1), np.int32)
+    after = np.zeros(max(rm.size, 1), np.uint64)
+    ptr = lambda a: a.ctypes.data if a.size else None
+    rc = lib().mori_replica_admit(b.size, ptr(b), ptr(it), ptr(st), rm.size, ptr(rm), flags, rep.ctypes.data,
+                                  after.ctypes.data)
+    return rc, rep[:b.size], after[:rm.size]

@@ -99,3 +99,15 @@ def ssd_cases():
             d[key] = int(kv[key])
         res[name] = d
     return res
+
+
+def replica_cases():
+    sections, _ = _kv_blocks(os.path.join(GOLDEN, "replica_worked.txt"))
+    res = {}
+    for name, kv in sections.items():
+        d = {k: [int(x) for x in kv[k].split()] for k in ("bytes", "room", "replica", "room_after")}
+        d["status"] = [STATUS[x] for x in kv["status"].split()]
+        d["idleness"] = [float(x) for x in kv["idleness"].split()]
+        d["best_fit"] = int(kv["best_fit"])
+        res[name] = d
+    return res
