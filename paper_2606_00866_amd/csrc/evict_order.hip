@@ -8,15 +8,20 @@
 // 64-bit key (type position << 62 | last access) with the block id riding
 // along, done here as a device-wide stable LSD radix sort:
 //
-//   keys     build keys, validate, OR/AND of all keys (digits on which every
-//            key agrees need no pass);
-//   per pass (8-bit digit, 8 passes)
-//     hist   per 4096-key tile: 256-bin histogram  -> hist[digit][tile]
-//     scan   one workgroup: exclusive scan of hist in (digit, tile) order
-//     scatter per tile: stable rank of every key among the tile's keys of its
-//            digit (wave64 ballots over the 8 digit bits, slices of 256 keys
-//            in original order) + the scanned base -> position
-//            (a pass over a constant digit copies instead);
+//   keys     build keys, validate, OR/AND of all keys;
+//   per pass (8-bit digit, 8 passes; a digit on which every key agrees needs
+//   no pass, and each kernel works out from the OR/AND which of the two
+//   key/value buffers holds the current order, so such a pass costs three
+//   empty launches and no memory traffic)
+//     hist   per tile of keys: 256-bin histogram  -> hist[digit][tile]
+//     dscan  one workgroup per digit: exclusive scan of that digit's counts
+//            over the tiles, and the digit's total
+//     scatter per tile: the digit bases (a 256-entry scan of the totals in
+//            LDS) + the tile's scanned count + the stable rank of every key
+//            among the tile's keys of its digit: wave64 ballots over the 8
+//            digit bits rank each key within its wave's 64 keys of a slice,
+//            one scan per digit over (slice, wave) in LDS orders the groups as
+//            the keys were ordered -> position (two barriers per tile);
 //   prefix   inclusive u64 scan of block bytes in eviction order (tile scans,
 //            one-workgroup scan of tile totals, fix-up) and the number of
 //            evictions that frees the requested bytes.
@@ -29,9 +34,12 @@ namespace mori {
 namespace {
 
 constexpr int ET = 256;                 // threads per tile workgroup
-constexpr int EIPT = 16;                // keys per thread
-constexpr int ETILE = ET * EIPT;        // 4096 keys per tile
 constexpr int ENW = ET / 64;            // waves per tile workgroup
+// Keys per thread (tile = 256 x that): measured on MI355X with the bench's
+// block metadata, 4 is fastest up to ~2^19 blocks (more workgroups for a
+// latency-bound sort), 8 above (fewer tiles to scan per digit).
+constexpr uint32_t SMALL_SORT = 1u << 19;
+inline int keys_per_thread(uint32_t N) { return N <= SMALL_SORT ? 4 : 8; }
 constexpr uint64_t TIME_LIMIT = 1ull << 62;
 
 struct EvictArgs {
@@ -43,6 +51,7 @@ struct EvictArgs {
   uint64_t* keys[2];
   uint32_t* vals[2];
   uint32_t* hist;       // [256][ntiles]
+  uint32_t* dtot;       // [256] keys per digit
   uint64_t* tile_sum;   // [ntiles]
   uint64_t* misc;       // [0] OR of keys, [1] AND of keys, [2] error bits, [3] evictions short of need
   uint32_t* order;      // out [N]
@@ -75,108 +84,149 @@ __global__ __launch_bounds__(ET) void evict_keys_kernel(EvictArgs a) {
     o |= key;
     n &= key;
   }
-  // wave-level reduction before the global atomics
+  // wave, then workgroup reduction: one set of global atomics per workgroup
+  __shared__ uint64_t s_red[3][ENW];
   for (int off = 32; off > 0; off >>= 1) {
     o |= __shfl_xor(o, off, 64);
     n &= __shfl_xor(n, off, 64);
     err |= __shfl_xor(err, off, 64);
   }
+  const int wid = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) {
+    s_red[0][wid] = o;
+    s_red[1][wid] = n;
+    s_red[2][wid] = err;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < ENW; ++w) {
+      o |= s_red[0][w];
+      n &= s_red[1][w];
+      err |= s_red[2][w];
+    }
     atomicOr((unsigned long long*)&a.misc[0], (unsigned long long)o);
     atomicAnd((unsigned long long*)&a.misc[1], (unsigned long long)n);
     if (err) atomicOr((unsigned long long*)&a.misc[2], (unsigned long long)err);
   }
 }
 
+__device__ inline uint64_t varying_bits(const EvictArgs& a) { return a.misc[0] ^ a.misc[1]; }
+
 __device__ inline bool digit_varies(const EvictArgs& a, int shift) {
-  return (((a.misc[0] ^ a.misc[1]) >> shift) & 255u) != 0;
+  return ((varying_bits(a) >> shift) & 255u) != 0;
 }
 
-__global__ __launch_bounds__(ET) void evict_hist_kernel(EvictArgs a, int src, int shift) {
+// Which buffer holds the order before the pass at `shift`: passes over
+// constant digits are skipped, so it is the parity of the varying digits below.
+__device__ inline int source_buffer(const EvictArgs& a, int shift) {
+  const uint64_t v = varying_bits(a);
+  int n = 0;
+  for (int s = 0; s < shift; s += 8) n += ((v >> s) & 255u) != 0;
+  return n & 1;
+}
+
+template <int EIPT>
+__global__ __launch_bounds__(ET) void evict_hist_kernel(EvictArgs a, int shift) {
   __shared__ uint32_t s_h[256];
   if (a.misc[2] || !digit_varies(a, shift)) return;
   s_h[threadIdx.x] = 0;
   __syncthreads();
-  const uint64_t* k = a.keys[src];
-  const uint64_t base = (uint64_t)blockIdx.x * ETILE;
-#pragma unroll 4
+  const uint64_t* k = a.keys[source_buffer(a, shift)];
+  const uint64_t base = (uint64_t)blockIdx.x * (ET * EIPT);
+  const uint64_t lanemask_lt = (1ull << (threadIdx.x & 63)) - 1ull;
+#pragma unroll
   for (int it = 0; it < EIPT; ++it) {
+    // keys of a program share their time, so digits repeat within a wave: one
+    // LDS increment per distinct digit (its first lane adds the group's size)
     const uint64_t i = base + it * ET + threadIdx.x;
-    if (i < a.N) atomicAdd(&s_h[(k[i] >> shift) & 255u], 1u);
+    const bool valid = i < a.N;
+    const uint32_t d = valid ? (uint32_t)(k[i] >> shift) & 255u : 0u;
+    uint64_t same = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const uint64_t bal = __ballot((d >> b) & 1u);
+      same &= ((d >> b) & 1u) ? bal : ~bal;
+    }
+    if (valid && (same & lanemask_lt) == 0) atomicAdd(&s_h[d], (uint32_t)__popcll(same));
   }
   __syncthreads();
   a.hist[(uint64_t)threadIdx.x * a.ntiles + blockIdx.x] = s_h[threadIdx.x];
 }
 
-// Exclusive scan of u32 counts in place (1024 threads); total fits in u32 (N < 2^32).
-__global__ __launch_bounds__(1024) void evict_scan_kernel(EvictArgs a, int shift) {
-  __shared__ uint32_t s_w[1024 / 64 + 1];
-  if (a.misc[2] || !digit_varies(a, shift)) return;
-  const uint64_t E = 256ull * a.ntiles;
+// Block-wide exclusive scan of one u32 per thread (256 threads); *total gets the sum.
+__device__ inline uint32_t scan256(uint32_t v, uint32_t* s_w, uint32_t* total) {
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  uint32_t carry = 0;
-  for (uint64_t e0 = 0; e0 < E; e0 += 1024) {
-    const uint64_t e = e0 + threadIdx.x;
-    const uint32_t v = e < E ? a.hist[e] : 0u;
-    uint32_t x = v;
+  uint32_t x = v;
 #pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const uint32_t y = __shfl_up(x, off, 64);
-      if (lane >= off) x += y;
-    }
-    if (lane == 63) s_w[wid] = x;
-    __syncthreads();
-    if (wid == 0) {
-      const uint32_t w = lane < 16 ? s_w[lane] : 0u;
-      uint32_t wi = w;
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) {
-        const uint32_t y = __shfl_up(wi, off, 64);
-        if (lane >= off) wi += y;
-      }
-      if (lane < 16) s_w[lane] = wi - w;
-      if (lane == 15) s_w[16] = wi;
-    }
-    __syncthreads();
-    if (e < E) a.hist[e] = carry + s_w[wid] + x - v;
-    carry += s_w[16];
-    __syncthreads();
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t y = __shfl_up(x, off, 64);
+    if (lane >= off) x += y;
   }
+  if (lane == 63) s_w[wid] = x;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < ENW; ++w) {
+    before += w < wid ? s_w[w] : 0u;
+    all += s_w[w];
+  }
+  __syncthreads();
+  *total = all;
+  return before + x - v;
 }
 
-__global__ __launch_bounds__(ET) void evict_scatter_kernel(EvictArgs a, int src, int shift) {
-  __shared__ uint32_t s_off[256];     // this tile's global base per digit
-  __shared__ uint32_t s_run[256];     // keys of each digit already placed by earlier slices
-  __shared__ uint32_t s_wc[ENW][256]; // per-slice, per-wave counts -> bases
-  if (a.misc[2]) return;
+// One workgroup per digit: exclusive scan of hist[digit][0..ntiles) in place
+// and the digit's total.
+__global__ __launch_bounds__(ET) void evict_dscan_kernel(EvictArgs a, int shift) {
+  __shared__ uint32_t s_w[ENW];
+  if (a.misc[2] || !digit_varies(a, shift)) return;
+  uint32_t* h = a.hist + (uint64_t)blockIdx.x * a.ntiles;
+  uint32_t carry = 0;
+  for (uint32_t t0 = 0; t0 < a.ntiles; t0 += ET) {
+    const uint32_t t = t0 + threadIdx.x;
+    const uint32_t v = t < a.ntiles ? h[t] : 0u;
+    uint32_t tot;
+    const uint32_t ex = scan256(v, s_w, &tot);
+    if (t < a.ntiles) h[t] = carry + ex;
+    carry += tot;
+  }
+  if (threadIdx.x == 0) a.dtot[blockIdx.x] = carry;
+}
+
+template <int EIPT>
+__global__ __launch_bounds__(ET) void evict_scatter_kernel(EvictArgs a, int shift) {
+  // s_cnt[slice][wave][digit]: keys of that digit in that wave's 64 keys of the
+  // slice, then (after the per-digit scan) their offset within the tile
+  __shared__ uint16_t s_cnt[EIPT][ENW][256];
+  __shared__ uint32_t s_off[256];  // this tile's global base per digit
+  __shared__ uint32_t s_w[ENW];
+  if (a.misc[2] || !digit_varies(a, shift)) return;
+  const int src = source_buffer(a, shift);
   const uint64_t* ks = a.keys[src];
   const uint32_t* vs = a.vals[src];
   uint64_t* kd = a.keys[src ^ 1];
   uint32_t* vd = a.vals[src ^ 1];
-  const uint64_t base = (uint64_t)blockIdx.x * ETILE;
-  if (!digit_varies(a, shift)) {  // every key has the same digit: the pass keeps the order
-    for (int it = 0; it < EIPT; ++it) {
-      const uint64_t i = base + it * ET + threadIdx.x;
-      if (i < a.N) {
-        kd[i] = ks[i];
-        vd[i] = vs[i];
-      }
-    }
-    return;
-  }
+  const uint64_t base = (uint64_t)blockIdx.x * (ET * EIPT);
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  s_off[tid] = a.hist[(uint64_t)tid * a.ntiles + blockIdx.x];
-  s_run[tid] = 0;
+  uint32_t tot;
+  const uint32_t digit_base = scan256(a.dtot[tid], s_w, &tot);
+  s_off[tid] = digit_base + a.hist[(uint64_t)tid * a.ntiles + blockIdx.x];
 #pragma unroll
-  for (int w = 0; w < ENW; ++w) s_wc[w][tid] = 0;
+  for (int it = 0; it < EIPT; ++it)
+#pragma unroll
+    for (int w = 0; w < ENW; ++w) s_cnt[it][w][tid] = 0;
   __syncthreads();
+  // rank of every key among the keys of its digit in its wave's slice (ballots)
   const uint64_t lanemask_lt = (1ull << lane) - 1ull;
+  uint64_t key[EIPT];
+  uint32_t val[EIPT], dig[EIPT], rnk[EIPT];
+#pragma unroll
   for (int it = 0; it < EIPT; ++it) {
     const uint64_t i = base + it * ET + tid;
     const bool valid = i < a.N;
-    const uint64_t key = valid ? ks[i] : 0ull;
-    const uint32_t val = valid ? vs[i] : 0u;
-    const uint32_t d = (uint32_t)(key >> shift) & 255u;
+    key[it] = valid ? ks[i] : 0ull;
+    val[it] = valid ? vs[i] : 0u;
+    const uint32_t d = (uint32_t)(key[it] >> shift) & 255u;
     uint64_t same = __ballot(valid);
 #pragma unroll
     for (int b = 0; b < 8; ++b) {
@@ -184,54 +234,67 @@ __global__ __launch_bounds__(ET) void evict_scatter_kernel(EvictArgs a, int src,
       same &= ((d >> b) & 1u) ? bal : ~bal;
     }
     const uint32_t r = __popcll(same & lanemask_lt);
-    if (valid && r == 0) s_wc[wid][d] = __popcll(same);
-    __syncthreads();
-    {  // bases of this slice: earlier slices, then earlier waves of this slice
-      uint32_t run = s_run[tid];
+    if (valid && r == 0) s_cnt[it][wid][d] = (uint16_t)__popcll(same);
+    dig[it] = valid ? d : 256u;
+    rnk[it] = r;
+  }
+  __syncthreads();
+  {  // per digit (one per thread): offsets in (slice, wave) order, i.e. original key order
+    uint32_t run = 0;
+#pragma unroll
+    for (int it = 0; it < EIPT; ++it)
 #pragma unroll
       for (int w = 0; w < ENW; ++w) {
-        const uint32_t c = s_wc[w][tid];
-        s_wc[w][tid] = run;
+        const uint32_t c = s_cnt[it][w][tid];
+        s_cnt[it][w][tid] = (uint16_t)run;
         run += c;
       }
-      s_run[tid] = run;
-    }
-    __syncthreads();
-    if (valid) {
-      const uint32_t pos = s_off[d] + s_wc[wid][d] + r;
-      kd[pos] = key;
-      vd[pos] = val;
-    }
-    __syncthreads();
+  }
+  __syncthreads();
 #pragma unroll
-    for (int w = 0; w < ENW; ++w) s_wc[w][tid] = 0;
-    __syncthreads();
+  for (int it = 0; it < EIPT; ++it) {
+    const uint32_t d = dig[it];
+    if (d < 256u) {
+      const uint32_t pos = s_off[d] + s_cnt[it][wid][d] + rnk[it];
+      kd[pos] = key[it];
+      vd[pos] = val[it];
+    }
   }
 }
 
 // Inclusive scan of freed bytes within each tile; tile totals to tile_sum.
-__global__ __launch_bounds__(ET) void evict_prefix_tiles_kernel(EvictArgs a, int src) {
+// Global memory is read and written in striped (coalesced) order and the
+// blocked per-thread scan runs on an LDS copy of the tile.
+template <int EIPT>
+__global__ __launch_bounds__(ET) void evict_prefix_tiles_kernel(EvictArgs a) {
+  __shared__ uint64_t s_b[ET * EIPT];
   __shared__ uint64_t s_w[ENW + 1];
   if (a.misc[2]) return;
-  const uint32_t* order = a.vals[src];
-  const uint64_t base = (uint64_t)blockIdx.x * ETILE + (uint64_t)threadIdx.x * EIPT;  // blocked: 16 consecutive
-  uint64_t v[EIPT];
-  uint64_t s = 0;
+  const uint32_t* order = a.vals[source_buffer(a, 64)];
+  const uint64_t base = (uint64_t)blockIdx.x * (ET * EIPT);
+  const int tid = threadIdx.x;
 #pragma unroll
-  for (int j = 0; j < EIPT; ++j) {
-    const uint64_t i = base + j;
+  for (int it = 0; it < EIPT; ++it) {
+    const uint64_t i = base + it * ET + tid;
     uint64_t bytes = 0;
     if (i < a.N) {
       const uint32_t b = order[i];
       a.order[i] = b;
       bytes = (uint64_t)(a.size ? a.size[b] : 1u) * a.unit_bytes;
     }
-    s += bytes;
-    v[j] = s;
+    s_b[it * ET + tid] = bytes;
+  }
+  __syncthreads();
+  uint64_t v[EIPT];
+  uint64_t sum = 0;
+#pragma unroll
+  for (int j = 0; j < EIPT; ++j) {  // blocked: keys tid * EIPT .. + EIPT - 1 of the tile
+    sum += s_b[tid * EIPT + j];
+    v[j] = sum;
   }
   // exclusive scan of the per-thread totals
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  uint64_t x = s;
+  const int lane = tid & 63, wid = tid >> 6;
+  uint64_t x = sum;
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
     const uint64_t y = __shfl_up(x, off, 64);
@@ -239,7 +302,7 @@ __global__ __launch_bounds__(ET) void evict_prefix_tiles_kernel(EvictArgs a, int
   }
   if (lane == 63) s_w[wid] = x;
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     uint64_t run = 0;
     for (int w = 0; w < ENW; ++w) {
       const uint64_t c = s_w[w];
@@ -249,11 +312,16 @@ __global__ __launch_bounds__(ET) void evict_prefix_tiles_kernel(EvictArgs a, int
     s_w[ENW] = run;
   }
   __syncthreads();
-  const uint64_t before = s_w[wid] + x - s;
+  const uint64_t before = s_w[wid] + x - sum;
 #pragma unroll
-  for (int j = 0; j < EIPT; ++j)
-    if (base + j < a.N) a.prefix[base + j] = before + v[j];
-  if (threadIdx.x == 0) a.tile_sum[blockIdx.x] = s_w[ENW];
+  for (int j = 0; j < EIPT; ++j) s_b[tid * EIPT + j] = before + v[j];
+  __syncthreads();
+#pragma unroll
+  for (int it = 0; it < EIPT; ++it) {
+    const uint64_t i = base + it * ET + tid;
+    if (i < a.N) a.prefix[i] = s_b[it * ET + tid];
+  }
+  if (tid == 0) a.tile_sum[blockIdx.x] = s_w[ENW];
 }
 
 __global__ __launch_bounds__(1024) void evict_prefix_top_kernel(EvictArgs a) {
@@ -290,10 +358,11 @@ __global__ __launch_bounds__(1024) void evict_prefix_top_kernel(EvictArgs a) {
   }
 }
 
+template <int EIPT>
 __global__ __launch_bounds__(ET) void evict_prefix_fix_kernel(EvictArgs a) {
   if (a.misc[2]) return;
   const uint64_t add = a.tile_sum[blockIdx.x];
-  const uint64_t base = (uint64_t)blockIdx.x * ETILE;
+  const uint64_t base = (uint64_t)blockIdx.x * (ET * EIPT);
   uint32_t short_of_need = 0;
   for (int it = 0; it < EIPT; ++it) {
     const uint64_t i = base + it * ET + threadIdx.x;
@@ -303,9 +372,15 @@ __global__ __launch_bounds__(ET) void evict_prefix_fix_kernel(EvictArgs a) {
       short_of_need += p < a.need;
     }
   }
+  __shared__ uint32_t s_short[ENW];
   for (int off = 32; off > 0; off >>= 1) short_of_need += __shfl_xor(short_of_need, off, 64);
-  if ((threadIdx.x & 63) == 0 && short_of_need)
-    atomicAdd((unsigned long long*)&a.misc[3], (unsigned long long)short_of_need);
+  if ((threadIdx.x & 63) == 0) s_short[threadIdx.x >> 6] = short_of_need;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t t = 0;
+    for (int w = 0; w < ENW; ++w) t += s_short[w];
+    if (t) atomicAdd((unsigned long long*)&a.misc[3], (unsigned long long)t);
+  }
 }
 
 __global__ void evict_result_kernel(EvictArgs a) {
@@ -319,13 +394,26 @@ __global__ void evict_result_kernel(EvictArgs a) {
   a.result[1] = (uint32_t)err;
 }
 
+template <int EIPT>
+void launch_tiles(const EvictArgs& a, hipStream_t s) {
+  for (int shift = 0; shift < 64; shift += 8) {
+    hipLaunchKernelGGL(evict_hist_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a, shift);
+    hipLaunchKernelGGL(evict_dscan_kernel, dim3(256), dim3(ET), 0, s, a, shift);
+    hipLaunchKernelGGL(evict_scatter_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a, shift);
+  }
+  hipLaunchKernelGGL(evict_prefix_tiles_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a);
+  hipLaunchKernelGGL(evict_prefix_top_kernel, dim3(1), dim3(1024), 0, s, a);
+  hipLaunchKernelGGL(evict_prefix_fix_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a);
+}
+
 }  // namespace
 
 uint64_t evict_workspace_bytes(uint32_t N) {
-  const uint64_t ntiles = ((uint64_t)N + ETILE - 1) / ETILE;
+  const uint64_t tile = (uint64_t)ET * keys_per_thread(N);
+  const uint64_t ntiles = ((uint64_t)N + tile - 1) / tile;
   auto up = [](uint64_t b) { return (b + 255) & ~255ull; };
-  return 2 * up(8ull * N) + 2 * up(4ull * N) + up(4ull * 256 * ntiles) + up(8ull * ntiles) + up(8ull * N) +
-         up(8 * 4);
+  return 2 * up(8ull * N) + 2 * up(4ull * N) + up(4ull * 256 * ntiles) + up(4 * 256) + up(8ull * ntiles) +
+         up(8ull * N) + up(8 * 4);
 }
 
 hipError_t launch_evict(uint32_t N, const uint8_t* type, const uint64_t* last_access, const uint32_t* size,
@@ -333,7 +421,9 @@ hipError_t launch_evict(uint32_t N, const uint8_t* type, const uint64_t* last_ac
                         uint64_t* prefix, uint32_t* result, hipStream_t s) {
   EvictArgs a{};
   a.N = N;
-  a.ntiles = (uint32_t)(((uint64_t)N + ETILE - 1) / ETILE);
+  const int kpt = keys_per_thread(N);
+  const uint64_t tile = (uint64_t)ET * kpt;
+  a.ntiles = (uint32_t)(((uint64_t)N + tile - 1) / tile);
   a.tier = tier;
   a.type = type;
   a.last_access = last_access;
@@ -352,6 +442,8 @@ hipError_t launch_evict(uint32_t N, const uint8_t* type, const uint64_t* last_ac
   w += up(4ull * N);
   a.hist = reinterpret_cast<uint32_t*>(w);
   w += up(4ull * 256 * a.ntiles);
+  a.dtot = reinterpret_cast<uint32_t*>(w);
+  w += up(4 * 256);
   a.tile_sum = reinterpret_cast<uint64_t*>(w);
   w += up(8ull * a.ntiles);
   uint64_t* prefix_tmp = reinterpret_cast<uint64_t*>(w);
@@ -362,20 +454,10 @@ hipError_t launch_evict(uint32_t N, const uint8_t* type, const uint64_t* last_ac
   a.result = result;
   const uint32_t tiles = a.ntiles ? a.ntiles : 1;
   hipLaunchKernelGGL(evict_init_kernel, dim3(1), dim3(1), 0, s, a);
-  hipLaunchKernelGGL(evict_keys_kernel, dim3(tiles < 2048 ? tiles * 4 : 8192), dim3(ET), 0, s, a);
-  int src = 0;
-  for (int shift = 0; shift < 64; shift += 8) {
-    if (a.ntiles) {
-      hipLaunchKernelGGL(evict_hist_kernel, dim3(a.ntiles), dim3(ET), 0, s, a, src, shift);
-      hipLaunchKernelGGL(evict_scan_kernel, dim3(1), dim3(1024), 0, s, a, shift);
-      hipLaunchKernelGGL(evict_scatter_kernel, dim3(a.ntiles), dim3(ET), 0, s, a, src, shift);
-    }
-    src ^= 1;
-  }
+  hipLaunchKernelGGL(evict_keys_kernel, dim3(tiles < 1024 ? tiles : 1024), dim3(ET), 0, s, a);
   if (a.ntiles) {
-    hipLaunchKernelGGL(evict_prefix_tiles_kernel, dim3(a.ntiles), dim3(ET), 0, s, a, src);
-    hipLaunchKernelGGL(evict_prefix_top_kernel, dim3(1), dim3(1024), 0, s, a);
-    hipLaunchKernelGGL(evict_prefix_fix_kernel, dim3(a.ntiles), dim3(ET), 0, s, a);
+    if (kpt == 4) launch_tiles<4>(a, s);
+    else launch_tiles<8>(a, s);
   }
   hipLaunchKernelGGL(evict_result_kernel, dim3(1), dim3(1), 0, s, a);
   return hipGetLastError();
