@@ -166,6 +166,7 @@ typedef struct {
   uint64_t pages_out, pages_in, pages_admit;
   uint64_t pages_free_before, pages_released, pages_recycled, pages_free_after;
   uint64_t bytes_out, bytes_in, gpu_bytes_after, cpu_bytes_after, ssd_bytes_after;
+  uint64_t pages_dropped; /* released pages of programs dropped to Waiting (nothing reads them) */
   const uint32_t* order;        /* [P] program ids, busiest first (incremental: see below) */
   const uint64_t* prefix;       /* [P] inclusive KV-byte prefix in rank order */
   const uint8_t* tier_old;      /* [P] */
@@ -212,6 +213,15 @@ int mori_host_free(void* ptr);
 /* Computes the new placement and rewrites tbl, tier and free_map in stream
  * order.  Waits (on the stream) for the previous plan's swaps.  The plan is
  * copied to the context's pinned mirror; read it with mori_plan_wait.
+ *
+ * Pages for programs entering the GPU are handed out in this order: pages
+ * free before the step, then pages of programs dropped to Waiting (nothing
+ * reads them), then pages of swapped-out programs (free once the swap-out has
+ * read them), each group in ascending page id; programs promoted from a lower
+ * tier take them first, then programs admitted from Waiting, each group in
+ * rank order, blocks in logical order.  A slot at or past pages_free_before +
+ * pages_dropped is on a page the swap-out reads: the swap-in waits for the
+ * swap-out before writing it, and the caller before prefilling it.
  *
  * Default policy (Sec. 4.3, Sec. 7.2): rank all programs by idleness (Eq. 1),
  * busiest first, and fill the GPU tier, then the CPU tier, from the busiest
@@ -269,7 +279,8 @@ int mori_kv_swap_out(mori_ctx* ctx, const uint64_t* host_dst, uint32_t mode, voi
 /* Swap-in of the last plan: for every program p with category IN, copies
  * host_src[p] + (q * nblk_p + i) * run_bytes into its newly allocated page of
  * block i, plane q.  Waits (on the stream) for the plan and, before writing a
- * page released by a swap-out of the same plan, for that swap-out.  The host
+ * page that the swap-out of the same plan reads, for that swap-out (pages
+ * free before the step and pages of dropped programs need no wait).  The host
  * buffers may be reused after it completes.  ESTATE: no plan, swap-in already
  * enqueued, or swap-out of the plan not yet enqueued. */
 int mori_kv_swap_in(mori_ctx* ctx, const uint64_t* host_src, uint32_t mode, void* stream);

@@ -416,7 +416,8 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
           continue;
         }
         page_state[pg] |= 2u;
-        if (cat[p] == ORC_OUT || cat[p] == ORC_DROP_GPU) page_state[pg] |= 4u;
+        if (cat[p] == ORC_DROP_GPU) page_state[pg] |= 4u;      /* released, nothing to read */
+        if (cat[p] == ORC_OUT) page_state[pg] |= 4u | 8u;      /* released once the swap-out read it */
       }
     }
     for (uint32_t pg = 0; pg < NB && rc == ORC_OK; ++pg)
@@ -428,17 +429,22 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
   }
 
   /* -- step 4: page allocation (Reading: pages free before this step in
-        ascending id order, then the pages released by programs leaving the
-        GPU in ascending id order; they are handed out first to the programs
-        promoted from the CPU tier, then to those admitted from Waiting,
-        following the promotion priority of Sec. 4.3.1, each group in rank
-        order, each program's blocks in logical order) -- */
-  uint64_t n_free0 = 0, n_rel = 0, need = 0;
+        ascending id order, then the pages of programs dropped from the GPU to
+        Waiting (nothing reads them), then the pages of programs swapped out
+        (free once the swap-out has read them), each group in ascending id
+        order; they are handed out first to the programs promoted from a lower
+        tier, then to those admitted from Waiting, following the promotion
+        priority of Sec. 4.3.1, each group in rank order, each program's
+        blocks in logical order) -- */
+  uint64_t n_free0 = 0, n_rel = 0, n_drop = 0, need = 0;
   if (rc == ORC_OK) {
     for (uint32_t pg = 0; pg < NB; ++pg)
       if (page_state[pg] & 1u) pages_avail[n_free0++] = pg;
     for (uint32_t pg = 0; pg < NB; ++pg)
-      if (page_state[pg] & 4u) pages_avail[n_free0 + n_rel++] = pg;
+      if ((page_state[pg] & 4u) && !(page_state[pg] & 8u)) pages_avail[n_free0 + n_rel++] = pg;
+    n_drop = n_rel;
+    for (uint32_t pg = 0; pg < NB; ++pg)
+      if (page_state[pg] & 8u) pages_avail[n_free0 + n_rel++] = pg;
     for (uint32_t p = 0; p < P; ++p)
       if (cat[p] == ORC_IN || cat[p] == ORC_ADMIT_GPU) need += nblk[p];
     if (need > n_free0 + n_rel) rc = ORC_E_NOSPC;
@@ -510,6 +516,7 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
       summary->pages_released = n_rel;
       summary->pages_recycled = need > n_free0 ? need - n_free0 : 0;
       summary->pages_free_after = n_free0 + n_rel - need;
+      summary->pages_dropped = n_drop;
       summary->bytes_out = summary->pages_out * block_bytes;
       summary->bytes_in = summary->pages_in * block_bytes;
     }

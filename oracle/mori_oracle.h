@@ -15,7 +15,9 @@
  *      the ranking until its byte budget is reached, then the CPU tier the same
  *      way; the rest waits (Sec. 4.1 three-tier queues, Sec. 4.3, Sec. 7.2);
  *   4. sticky placement: only programs whose tier changes move (Sec. 4.3), with
- *      KV pages of paged attention (Sec. 2.1) allocated lowest id first;
+ *      KV pages of paged attention (Sec. 2.1) allocated lowest id first, pages
+ *      free before the step ahead of released ones and, among those, pages
+ *      nothing reads ahead of pages a swap-out reads;
  *   5. the byte movement this implies: demoted programs' pages copied into
  *      their contiguous host buffers, promoted programs' bytes copied back into
  *      newly allocated pages (Sec. 4.1: the CPU tier resumes over PCIe).
@@ -85,6 +87,7 @@ typedef struct {
   uint64_t pages_out, pages_in, pages_admit;
   uint64_t pages_free_before, pages_released, pages_recycled, pages_free_after;
   uint64_t bytes_out, bytes_in, gpu_bytes_after, cpu_bytes_after, ssd_bytes_after;
+  uint64_t pages_dropped; /* released pages of programs dropped to Waiting: reusable at once */
 } orc_summary;
 
 /* Eq. 1 for every program.  window is [P][k][2] (reasoning s, acting s), oldest first. */

@@ -55,7 +55,7 @@ class _Summary(C.Structure):
         (n, C.c_uint64) for n in (
             "pages_out", "pages_in", "pages_admit", "pages_free_before", "pages_released",
             "pages_recycled", "pages_free_after", "bytes_out", "bytes_in", "gpu_bytes_after",
-            "cpu_bytes_after", "ssd_bytes_after")]
+            "cpu_bytes_after", "ssd_bytes_after", "pages_dropped")]
 
 
 _lib = None

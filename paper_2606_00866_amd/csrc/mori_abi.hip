@@ -11,11 +11,12 @@
 //              the context's copy stream, while the next gather fills the
 //              other half.
 //   swap-in    direct: translate -> scatter of slots on pages free before the
-//              step -> wait for the swap-out -> scatter of recycled slots;
-//              copy engine: per chunk, hipMemcpyAsync host -> staging half on
-//              the copy stream -> scatter kernel on the caller's stream (after
-//              the swap-out event from the first chunk that writes a recycled
-//              page), the next chunk loading into the other half meanwhile.
+//              step or released by dropped programs -> wait for the swap-out ->
+//              scatter of slots on pages it has read; copy engine: per chunk,
+//              hipMemcpyAsync host -> staging half on the copy stream -> scatter
+//              kernel on the caller's stream (after the swap-out event from the
+//              first chunk that writes a page the swap-out reads), the next
+//              chunk loading into the other half meanwhile.
 //   next plan  waits on the stream for both swaps of the previous plan.
 #include <hip/hip_runtime.h>
 
@@ -210,7 +211,7 @@ extern "C" int mori_create(const mori_pool* pool, uint32_t max_programs, uint64_
     return r;
   };
   const size_t o_base = take(4 * pm), o_pstate = take(4 * NB), o_out_src = take(4 * NB), o_in_dst = take(4 * NB);
-  const size_t o_tc = take(8ull * c->ntiles), o_tb = take(8ull * c->ntiles);
+  const size_t o_tc = take(16ull * c->ntiles), o_tb = take(16ull * c->ntiles);
   const size_t o_as0 = take(8 * pm), o_as1 = take(8 * pm), o_ad0 = take(8 * pm), o_ad1 = take(8 * pm);
   const size_t o_err = take(4), o_rng = take(sizeof(DevRange) * MORI_MAX_RANGES);
   if ((e = hipMalloc(&c->scratch, o)) != hipSuccess) return fail(e);
@@ -388,6 +389,7 @@ extern "C" int mori_plan_wait(mori_ctx* ctx, mori_plan* out) {
   p.pages_free_before = s->pages_free_before;
   p.pages_released = s->pages_released;
   p.pages_recycled = s->pages_recycled;
+  p.pages_dropped = s->pages_dropped;
   p.pages_free_after = s->pages_free_after;
   p.bytes_out = s->bytes_out;
   p.bytes_in = s->bytes_in;
@@ -604,13 +606,15 @@ extern "C" int mori_kv_swap_in(mori_ctx* ctx, const uint64_t* host_src, uint32_t
     const uint32_t* base = ctx->host<uint32_t>(ctx->L.in_base);
     if (!host_check(ctx, host_src, progs, n, base)) return MORI_EINVAL;
     HIP_TRY(ctx, hipStreamWaitEvent(s, ctx->ev_plan, 0));
-    const uint64_t LC = ctx->LC, run = ctx->run, nf = sh->pages_free_before;
+    // slots below `ready` are on pages free before the step or released by a
+    // dropped program; the rest are on pages the swap-out reads first
+    const uint64_t LC = ctx->LC, run = ctx->run, ready = sh->pages_free_before + sh->pages_dropped;
     const uint64_t total = n ? (uint64_t)base[n] * LC : 0;
     const uint64_t cu = ctx->staging_bytes / 2 / run;  // chunk = one staging half
-    // first unit of the first program with a slot on a released page
+    // first unit of the first program with a slot on a page the swap-out reads
     uint64_t u_recycled = total;
     for (uint32_t k = 0; k < n; ++k)
-      if (base[k + 1] > nf && base[k + 1] > base[k]) {
+      if (base[k + 1] > ready && base[k + 1] > base[k]) {
         u_recycled = (uint64_t)base[k] * LC;
         break;
       }

@@ -12,6 +12,7 @@ namespace mori {
 constexpr uint32_t PS_FREE = 1u;   // marked free in the caller's free map before the step
 constexpr uint32_t PS_OWNED = 2u;  // owned by a GPU-resident program
 constexpr uint32_t PS_REL = 4u;    // owned by a program leaving the GPU this step
+constexpr uint32_t PS_COPY = 8u;   // ... whose KV the swap-out reads from it first
 
 constexpr int PAGE_TILE = 4096;    // pages per workgroup in the page-allocation kernels
 constexpr int PAGE_WG = 256;       // threads per page-allocation workgroup (16 pages each)
@@ -25,6 +26,7 @@ struct DevSummary {
   uint64_t pages_free_before, pages_released, pages_recycled, pages_free_after;
   uint64_t bytes_out, bytes_in, gpu_bytes_after, cpu_bytes_after, ssd_bytes_after;
   uint64_t need;  // pages_in + pages_admit
+  uint64_t pages_dropped;  // released pages nothing reads: slots below free-before + this need no wait
 };
 
 // A registered memory range usable by the swap kernels.
@@ -63,8 +65,8 @@ struct PlanArgs {
   uint32_t* pstate;       // [NB]
   uint32_t* out_src;      // [pages_out] old page of each out page index
   uint32_t* in_dst;       // [need] page of each slot
-  uint64_t* tile_cnt;     // [ntiles] packed (free-before count, released count << 32)
-  uint64_t* tile_base;    // [ntiles] exclusive prefix of tile_cnt
+  uint64_t* tile_cnt;     // [2 ntiles]: packed (free-before, dropped << 32), then swapped-out counts
+  uint64_t* tile_base;    // [2 ntiles] exclusive prefixes of both halves of tile_cnt
   uint32_t* swap_err;     // cleared by every plan
 };
 

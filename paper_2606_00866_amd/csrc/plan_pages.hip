@@ -6,12 +6,15 @@
 //            twice, none both owned and free, none out of range, no page held
 //            by a CPU/Waiting program), mark pages of programs leaving the
 //            GPU as released, record the old page of every swap-out block;
-//   count    per 4096-page tile: pages free before the step and released
-//            pages; a page that is neither free nor owned is a leak;
+//   count    per 4096-page tile: pages free before the step, released pages
+//            of dropped programs, released pages of swapped-out programs; a
+//            page that is neither free nor owned is a leak;
 //   scan     one workgroup: exclusive prefix over tiles, totals, capacity;
 //   assign   slot j of the incoming programs takes the j-th page of
-//            (free-before ascending ++ released ascending); the free map after
-//            the step is what is left of that sequence;
+//            (free-before ++ dropped ++ swapped out, each ascending): pages
+//            nothing reads come before pages the swap-out reads, so the
+//            swap-in waits only for slots past the first two groups; the free
+//            map after the step is what is left of that sequence;
 //   commit   rewrite the block tables (released -> no page, incoming -> their
 //            slots' pages) and the tier vector.
 //
@@ -59,8 +62,8 @@ __global__ __launch_bounds__(WG) void pages_claim_kernel(PlanArgs a) {
       continue;
     }
     const uint8_t c = a.cat[p];
-    const bool leaves = (c == MORI_CAT_OUT) || (c == MORI_CAT_DROP_GPU);
-    const uint32_t old = atomicOr(&a.pstate[pg], PS_OWNED | (leaves ? PS_REL : 0u));
+    const uint32_t leaves = c == MORI_CAT_OUT ? (PS_REL | PS_COPY) : c == MORI_CAT_DROP_GPU ? PS_REL : 0u;
+    const uint32_t old = atomicOr(&a.pstate[pg], PS_OWNED | leaves);
     if (old & (PS_FREE | PS_OWNED)) err |= MORI_DEV_PAGE_DUP;
     if (c == MORI_CAT_OUT) {
       const uint32_t k = a.base[p] + (e - a.tbl_off[p]);
@@ -72,27 +75,30 @@ __global__ __launch_bounds__(WG) void pages_claim_kernel(PlanArgs a) {
 }
 
 __global__ __launch_bounds__(WG) void pages_count_kernel(PlanArgs a) {
-  __shared__ uint32_t s_free, s_rel, s_err;
+  __shared__ uint32_t s_free, s_drop, s_copy, s_err;
   if (a.sum->error) return;
-  if (threadIdx.x == 0) s_free = s_rel = s_err = 0;
+  if (threadIdx.x == 0) s_free = s_drop = s_copy = s_err = 0;
   __syncthreads();
   const uint32_t per = PAGE_TILE / WG;
   const uint64_t start = (uint64_t)blockIdx.x * PAGE_TILE + (uint64_t)threadIdx.x * per;
-  uint32_t nf = 0, nr = 0, err = 0;
+  uint32_t nf = 0, nd = 0, nc = 0, err = 0;
   for (uint32_t j = 0; j < per; ++j) {
     const uint64_t pg = start + j;
     if (pg >= a.NB) break;
     const uint32_t st = a.pstate[pg];
     if (st == PS_FREE) ++nf;
-    else if (st & PS_REL) ++nr;
+    else if (st & PS_COPY) ++nc;
+    else if (st & PS_REL) ++nd;
     else if (st == 0) err |= MORI_DEV_PAGE_LEAK;
   }
   if (nf) atomicAdd(&s_free, nf);
-  if (nr) atomicAdd(&s_rel, nr);
+  if (nd) atomicAdd(&s_drop, nd);
+  if (nc) atomicAdd(&s_copy, nc);
   if (err) atomicOr(&s_err, err);
   __syncthreads();
   if (threadIdx.x == 0) {
-    a.tile_cnt[blockIdx.x] = (uint64_t)s_free | ((uint64_t)s_rel << 32);
+    a.tile_cnt[blockIdx.x] = (uint64_t)s_free | ((uint64_t)s_drop << 32);
+    a.tile_cnt[a.ntiles + blockIdx.x] = s_copy;
     if (s_err) atomicOr(&a.sum->error, s_err);
   }
 }
@@ -131,25 +137,30 @@ __device__ uint64_t wg_scan_excl(uint64_t v, uint64_t* s_wave, uint64_t* total) 
 __global__ __launch_bounds__(1024) void pages_scan_kernel(PlanArgs a) {
   __shared__ uint64_t s_wave[1024 / 64 + 1];
   if (a.sum->error) return;
-  uint64_t carry = 0;
-  for (uint32_t t0 = 0; t0 < a.ntiles; t0 += 1024) {
-    const uint32_t t = t0 + threadIdx.x;
-    const uint64_t v = t < a.ntiles ? a.tile_cnt[t] : 0ull;
-    uint64_t tot;
-    const uint64_t ex = wg_scan_excl<1024>(v, s_wave, &tot);
-    if (t < a.ntiles) a.tile_base[t] = carry + ex;
-    carry += tot;
+  uint64_t carry[2] = {0, 0};
+  for (int half = 0; half < 2; ++half) {  // (free-before | dropped << 32), then swapped out
+    const uint64_t* cnt = a.tile_cnt + (uint64_t)half * a.ntiles;
+    uint64_t* out = a.tile_base + (uint64_t)half * a.ntiles;
+    for (uint32_t t0 = 0; t0 < a.ntiles; t0 += 1024) {
+      const uint32_t t = t0 + threadIdx.x;
+      const uint64_t v = t < a.ntiles ? cnt[t] : 0ull;
+      uint64_t tot;
+      const uint64_t ex = wg_scan_excl<1024>(v, s_wave, &tot);
+      if (t < a.ntiles) out[t] = carry[half] + ex;
+      carry[half] += tot;
+    }
   }
   if (threadIdx.x == 0) {
     DevSummary* s = a.sum;
-    const uint64_t nf = carry & 0xFFFFFFFFull, rel = carry >> 32;
+    const uint64_t nf = carry[0] & 0xFFFFFFFFull, nd = carry[0] >> 32, nc = carry[1];
     s->pages_free_before = nf;
-    s->pages_released = rel;
-    if (s->need > nf + rel) {
+    s->pages_released = nd + nc;
+    s->pages_dropped = nd;
+    if (s->need > nf + nd + nc) {
       atomicOr(&s->error, MORI_DEV_NOSPC);
     } else {
       s->pages_recycled = s->need > nf ? s->need - nf : 0;
-      s->pages_free_after = nf + rel - s->need;
+      s->pages_free_after = nf + nd + nc - s->need;
     }
   }
 }
@@ -160,26 +171,30 @@ __global__ __launch_bounds__(WG) void pages_assign_kernel(PlanArgs a) {
   const uint32_t per = PAGE_TILE / WG;
   const uint64_t start = (uint64_t)blockIdx.x * PAGE_TILE + (uint64_t)threadIdx.x * per;
   uint32_t st[PAGE_TILE / WG];
-  uint32_t nf = 0, nr = 0;
+  uint32_t nf = 0, nd = 0, nc = 0;
 #pragma unroll
   for (uint32_t j = 0; j < per; ++j) {
     const uint64_t pg = start + j;
     st[j] = pg < a.NB ? a.pstate[pg] : PS_OWNED;
     if (st[j] == PS_FREE) ++nf;
-    else if (st[j] & PS_REL) ++nr;
+    else if (st[j] & PS_COPY) ++nc;
+    else if (st[j] & PS_REL) ++nd;
   }
   uint64_t tot;
-  const uint64_t ex = wg_scan_excl<WG>((uint64_t)nf | ((uint64_t)nr << 32), s_wave, &tot);
-  const uint64_t tb = a.tile_base[blockIdx.x];
+  const uint64_t ex = wg_scan_excl<WG>((uint64_t)nf | ((uint64_t)nd << 32), s_wave, &tot);
+  const uint64_t exc = wg_scan_excl<WG>(nc, s_wave, &tot);
+  const uint64_t tb = a.tile_base[blockIdx.x], tbc = a.tile_base[a.ntiles + blockIdx.x];
   uint64_t fi = (tb & 0xFFFFFFFFull) + (ex & 0xFFFFFFFFull);
-  uint64_t ri = (tb >> 32) + (ex >> 32);
-  const uint64_t nf_all = a.sum->pages_free_before, need = a.sum->need;
+  uint64_t di = (tb >> 32) + (ex >> 32);
+  uint64_t ci = tbc + exc;
+  const uint64_t nf_all = a.sum->pages_free_before, nd_all = a.sum->pages_dropped, need = a.sum->need;
 #pragma unroll
   for (uint32_t j = 0; j < per; ++j) {
     const uint64_t pg = start + j;
     uint64_t slot;
     if (st[j] == PS_FREE) slot = fi++;
-    else if (st[j] & PS_REL) slot = nf_all + ri++;
+    else if (st[j] & PS_COPY) slot = nf_all + nd_all + ci++;
+    else if (st[j] & PS_REL) slot = nf_all + di++;
     else continue;
     if (slot < need) {
       a.in_dst[slot] = (uint32_t)pg;

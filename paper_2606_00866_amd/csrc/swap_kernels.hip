@@ -15,9 +15,11 @@
 //   swap_in  : host buffer (direct) or staging -> newly allocated pool page
 //
 // Swap-in is launched in two parts in direct mode: slots taken from pages
-// that were free before the step, which no swap-out reads, and slots taken
-// from pages released this step, which must wait for the swap-out (the host
-// orders the second part after the swap-out's completion event).
+// that were free before the step or released by programs dropped to Waiting,
+// which no swap-out reads, and slots taken from pages of swapped-out
+// programs, which must wait for the swap-out (the host orders the second part
+// after the swap-out's completion event).  Page allocation hands out the
+// first kind first, so the split is one slot index.
 #include "mori_internal.h"
 
 namespace mori {
@@ -68,7 +70,7 @@ template <bool kOut>
 __device__ inline bool unit_range(const SwapArgs& s, uint32_t n, uint64_t* lo, uint64_t* hi) {
   const uint64_t LC = s.LC;
   const uint64_t total = (uint64_t)s.pg_base[n] * LC;
-  const uint64_t nf = s.sum->pages_free_before;
+  const uint64_t nf = s.sum->pages_free_before + s.sum->pages_dropped;  // slots needing no wait
   *lo = 0;
   *hi = total;
   if (s.staging) {
@@ -102,7 +104,7 @@ __device__ inline bool unit_ends(const SwapArgs& s, uint32_t n, uint64_t u, uint
   const uint64_t q = rem / nb, i = rem - q * nb;
   const uint64_t slot = first + i;
   if (!kOut && s.part != 0) {
-    const uint64_t nf = s.sum->pages_free_before;
+    const uint64_t nf = s.sum->pages_free_before + s.sum->pages_dropped;
     if ((s.part == 1) != (slot < nf)) return false;
   }
   uint8_t* pool_run = s.pool + (q * s.NB + s.pages[slot]) * s.run;

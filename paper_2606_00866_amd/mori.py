@@ -62,7 +62,8 @@ class mori_plan(C.Structure):
         "num_programs", "m_gpu", "m_cpu", "n_out", "n_in", "n_drop_gpu", "n_drop_cpu", "n_admit_gpu",
         "n_admit_cpu", "device_error", "m_ssd")] + [(n, C.c_uint64) for n in (
             "pages_out", "pages_in", "pages_admit", "pages_free_before", "pages_released", "pages_recycled",
-            "pages_free_after", "bytes_out", "bytes_in", "gpu_bytes_after", "cpu_bytes_after", "ssd_bytes_after")] + [
+            "pages_free_after", "bytes_out", "bytes_in", "gpu_bytes_after", "cpu_bytes_after", "ssd_bytes_after",
+            "pages_dropped")] + [
         ("order", C.POINTER(C.c_uint32)), ("prefix", C.POINTER(C.c_uint64)), ("tier_old", C.POINTER(C.c_uint8)),
         ("tier_new", C.POINTER(C.c_uint8)), ("category", C.POINTER(C.c_uint8)),
         ("out_programs", C.POINTER(C.c_uint32)), ("in_programs", C.POINTER(C.c_uint32))]

@@ -56,11 +56,17 @@ def _check_invariants(orc, inst, res, tbl0, tier0, free0, tbl, tier, free, budge
     for p in range(P):
         if tier[p] == tier0[p]:
             assert (tbl[off[p]:off[p + 1]] == tbl0[off[p]:off[p + 1]]).all()
-    # allocation: the pages handed out are the lowest ids of (free-before ++ released)
+    # allocation: pages handed out in the order free-before ++ dropped ++ swapped out, each ascending
     f0 = np.flatnonzero(free0)
-    rel = np.sort(np.concatenate([tbl0[off[p]:off[p + 1]] for p in range(P)
-                                  if tier0[p] == 0 and tier[p] != 0] + [np.zeros(0, np.uint32)]))
-    avail = np.concatenate([f0, rel]).astype(np.int64)
+
+    def pages_of(leaving_to):
+        return np.sort(np.concatenate([tbl0[off[p]:off[p + 1]] for p in range(P)
+                                       if tier0[p] == 0 and tier[p] in leaving_to] + [np.zeros(0, np.uint32)]))
+
+    dropped = pages_of((2,))      # nothing reads them
+    swapped = pages_of((1, 3))    # free once the swap-out has read them
+    avail = np.concatenate([f0, dropped, swapped]).astype(np.int64)
+    assert res.summary["pages_dropped"] == dropped.size
     incoming = [p for p in res.order if tier0[p] == 1 and tier[p] == 0] + \
                [p for p in res.order if tier0[p] == 2 and tier[p] == 0]
     got = np.concatenate([tbl[off[p]:off[p + 1]] for p in incoming] + [np.zeros(0, np.uint32)]).astype(np.int64)
