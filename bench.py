@@ -53,6 +53,11 @@ def parse():
     ap.add_argument("--steps", type=int, default=6)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="llama3_8b")
+    ap.add_argument("--scale", type=float, default=None,
+                    help="context scale (churn: default 0.32, a ~120 GiB pool; others: 1)")
+    ap.add_argument("--schedule", default="reverse", choices=["reverse", "rotate"],
+                    help="reverse: steps alternate drawn and reversed windows; rotate: each step the CPU-tier "
+                         "programs become the busiest (idleness given), so both directions move every step")
     ap.add_argument("--mode", default="auto", choices=["auto", "kernel", "ce"])
     ap.add_argument("--arena-gib", type=float, default=60.0, help="pinned CPU-tier arena")
     ap.add_argument("--cpu-gib", type=float, default=28.0, help="CPU-tier budget")
@@ -347,16 +352,21 @@ def main() -> int:
 
     from paper_2606_00866_amd import mori as M
     from paper_2606_00866_amd.tiering import TierPool, check
-    from workload import CONFIGS, budget_bytes, fill_pool_torch, make_bank, make_instance, run_content
+    from workload import CONFIGS, budget_bytes, churn_steps, fill_pool_torch, make_bank, make_instance, run_content
 
     cfg = CONFIGS[args.workload]
     M.lib()
     assert torch.cuda.is_available(), "bench.py needs the GPU"
-    inst = make_instance(cfg)
+    churn = cfg.name == "churn"  # 1024 programs, nothing placed yet, budget swinging, phases flipping
+    scale = args.scale if args.scale is not None else (0.32 if churn else 1.0)
+    inst = make_instance(cfg, scale=scale, resident="wait" if churn else "gpu")
     g = inst.geom
     total = inst.total_bytes
     bg = budget_bytes(total, cfg.gpu_pct)
     bc = int(args.cpu_gib * GIB)
+    # churn: step 0 places the first partition; step t >= 1 takes the t-th budget and windows
+    churn_inputs = ([(budget_bytes(total, pct), w) for _, pct, _, w in
+                     churn_steps(cfg, inst.busy, steps=args.warmup + args.steps)] if churn else None)
     log(f"workload {cfg.name}: P={inst.P} NB={g.num_blocks} block={g.block_bytes} B total={total / GIB:.2f} GiB "
         f"gpu_budget={bg / GIB:.2f} GiB cpu_budget={bc / GIB:.2f} GiB")
 
@@ -386,6 +396,10 @@ def main() -> int:
                   max_programs=inst.P, staging_bytes=args.staging_mib << 20, pool=pool)
     mode = {"auto": M.MORI_COPY_AUTO, "kernel": M.MORI_COPY_KERNEL, "ce": M.MORI_COPY_CE}[args.mode]
     wins = [torch.from_numpy(inst.window).cuda(), torch.from_numpy(inst.window[:, :, ::-1].copy()).cuda()]
+    rot_levels = torch.tensor([0.5, 0.1, 0.9], dtype=torch.float32, device="cuda")  # indexed by tier
+    if churn:
+        churn_inputs = [(b, torch.from_numpy(np.ascontiguousarray(w)).cuda()) for b, w in churn_inputs]
+    step_bg = [bg]  # the GPU budget of the last step
     history = []
     valid = np.ones(inst.P, bool)  # programs whose KV bytes are defined (never re-admitted from Waiting)
 
@@ -394,7 +408,17 @@ def main() -> int:
     def one_step(t, timed=False):
         e0, e_plan, e_out, e_in = (torch.cuda.Event(enable_timing=True) for _ in range(4))
         e0.record(s_out)
-        check(tp.rank_partition(gpu_bytes=bg, cpu_bytes=bc, window=wins[t % 2], stream=s_out), "rank")
+        if churn:
+            bg_t, w_t = (bg, wins[0]) if t == 0 else churn_inputs[t - 1]
+            step_bg[0] = bg_t
+            check(tp.rank_partition(gpu_bytes=bg_t, cpu_bytes=bc, window=w_t, stream=s_out), "rank")
+        elif args.schedule == "rotate":  # CPU tier busiest, then GPU tier, Waiting last
+            with torch.cuda.stream(s_out):
+                iota = rot_levels[tp.tier.long()]
+            check(tp.rank_partition(gpu_bytes=bg, cpu_bytes=bc, idleness=iota, flags=M.MORI_F_IDLENESS_GIVEN,
+                                    stream=s_out), "rank")
+        else:
+            check(tp.rank_partition(gpu_bytes=bg, cpu_bytes=bc, window=wins[t % 2], stream=s_out), "rank")
         e_plan.record(s_out)
         rc, p = tp.plan_wait()
         if rc != M.MORI_OK:
@@ -451,7 +475,7 @@ def main() -> int:
 
     verify = None
     if not args.no_verify:
-        verify = verify_sampled(inst, tp, bank, history, bg, bc, valid, np, run_content)
+        verify = verify_sampled(inst, tp, bank, history, step_bg[0], bc, valid, np, run_content)
         log(f"verify: {verify}")
 
     evict = None if args.no_evict else evict_leg(torch, np, M, evict_sizes)
@@ -476,10 +500,14 @@ def main() -> int:
         "data": "synthetic",
         "config": {
             "workload": (f"{cfg.name}: {inst.P} programs, {cfg.layers} layers x {cfg.planes} planes x "
-                         f"{cfg.row_bytes} B rows (8 KV heads x 128 bf16), {cfg.block_tokens}-token blocks, "
+                         f"{cfg.row_bytes} B rows ({cfg.dtype}), {cfg.block_tokens}-token blocks, "
                          f"{g.num_blocks} pages = {g.pool_bytes / GIB:.2f} GiB pool, GPU budget {cfg.gpu_pct}% "
                          f"of KV bytes, CPU tier {args.cpu_gib:g} GiB in a {args.arena_gib:g} GiB pinned arena; "
-                         f"steps alternate drawn / reversed idleness windows"),
+                         + (f"contexts scaled by {scale:g}, nothing placed before step 0, then per step the GPU "
+                            f"budget swings {cfg.pct_swing[0]:g}+-{cfg.pct_swing[1]:g}% and "
+                            f"{cfg.flip_frac:.0%} of programs flip phase" if churn else
+                            "steps alternate drawn / reversed idleness windows" if args.schedule == "reverse" else
+                            "each step the CPU-tier programs become the busiest (idleness given)")),
             "copy_mode": {0: "auto", 1: "kernel", 2: "copy-engine"}[int(last_mode)],
             "hw_queues": int(os.environ["GPU_MAX_HW_QUEUES"]),
             "gpu_budget_bytes": bg,
