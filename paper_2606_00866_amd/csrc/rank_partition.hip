@@ -1,4 +1,4 @@
-// Rank / boundary step of one rebalance, in a single 1024-thread workgroup.
+// Rank / boundary step of one rebalance, in a single workgroup.
 //
 //   1. idleness of every program by Eq. 1 (Sec. 4.2), binary32, totals
 //      accumulated oldest cycle first from +0, correctly rounded division;
@@ -27,19 +27,17 @@
 namespace mori {
 namespace {
 
-constexpr int RT = 1024;           // threads
-constexpr int IPT = 4;             // items per thread, striped: item x = it * RT + tid
-constexpr int NW = RT / 64;        // wavefronts
+// Three shapes, chosen by P at launch: 256 threads x 1 item for P <= 256
+// (barriers over 4 waves), 1024 x 1 up to 1024 and 1024 threads x 4 items
+// (striped: item x = it * RT + tid) up to 4096; fewer item slices mean fewer
+// workgroup scans, which dominate this latency-bound step.
 constexpr int RADIX_BITS = 4;
 constexpr int RADIX = 1 << RADIX_BITS;
 constexpr int KEY_BITS = 64;
 constexpr int GROUP_SHIFT = 61;  // incremental keys: listing group in the top three bits
-static_assert(RT * IPT == (int)MORI_MAX_PROGRAMS, "one key per thread slot");
-static_assert(RADIX * IPT * NW == RT, "one digit counter per thread");
-
-// Exclusive scan of one value per thread over the whole workgroup (thread
-// order); *total receives the sum.  s_wave needs NW + 1 entries.
-template <typename T>
+// Exclusive scan of one value per thread over the whole workgroup of NW
+// waves (thread order); *total receives the sum.  s_wave needs NW + 1 entries.
+template <int NW, typename T>
 __device__ T block_scan_excl(T v, T* s_wave, T* total) {
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   T x = v;
@@ -83,7 +81,10 @@ __device__ inline uint8_t category(uint8_t from, uint8_t to) {
   }
 }
 
+template <int RT, int IPT>
 __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
+  constexpr int NW = RT / 64;  // wavefronts
+  static_assert(RADIX * IPT * NW <= RT, "one digit counter per thread");
   __shared__ uint64_t s_key[RT * IPT];  // sort scratch, then the inclusive byte prefix by rank
   __shared__ uint32_t s_id[RT * IPT];   // sort scratch, then blocks by rank
   __shared__ uint32_t s_cnt[RT];
@@ -221,7 +222,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     }
     __syncthreads();
     uint32_t tot;
-    const uint32_t base = block_scan_excl<uint32_t>(s_cnt[tid], s_w32, &tot);
+    const uint32_t base = block_scan_excl<NW, uint32_t>(s_cnt[tid], s_w32, &tot);
     s_cnt[tid] = base;
     __syncthreads();
 #pragma unroll
@@ -258,7 +259,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
   for (int it = 0; it < IPT; ++it) {
     const uint64_t bytes = (uint64_t)nb[it] * a.block_bytes;
     uint64_t tot;
-    const uint64_t ex = block_scan_excl<uint64_t>(bytes, s_w64, &tot);
+    const uint64_t ex = block_scan_excl<NW, uint64_t>(bytes, s_w64, &tot);
     S[it] = carry + ex + bytes;
     carry += tot;
     const uint32_t r = it * RT + tid;
@@ -318,7 +319,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
         const bool cand = (r >= g1 && r < c_end) || (r >= g2 && r < g4);
         const uint64_t cb = cand ? (uint64_t)nb[it] * a.block_bytes : 0;
         uint64_t tot;
-        const uint64_t T = ccarry + block_scan_excl<uint64_t>(cb, s_w64, &tot) + cb;
+        const uint64_t T = ccarry + block_scan_excl<NW, uint64_t>(cb, s_w64, &tot) + cb;
         ccarry += tot;
         if (cand && T <= room_gpu) s_tier[r] = MORI_TIER_GPU;
       }
@@ -472,8 +473,8 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
       if (tnew == MORI_TIER_SSD) ssd_after += (uint64_t)nb[it] * a.block_bytes;
     }
     uint64_t tA, tB;
-    exA[it] = carryA + block_scan_excl<uint64_t>(va, s_w64, &tA);
-    exB[it] = carryB + block_scan_excl<uint64_t>(vb, s_w64, &tB);
+    exA[it] = carryA + block_scan_excl<NW, uint64_t>(va, s_w64, &tA);
+    exB[it] = carryB + block_scan_excl<NW, uint64_t>(vb, s_w64, &tB);
     carryA += tA;
     carryB += tB;
   }
@@ -542,7 +543,10 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
 }  // namespace
 
 hipError_t launch_rank(const PlanArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(rank_partition_kernel, dim3(1), dim3(RT), 0, s, a);
+  static_assert(1024 * 4 == (int)MORI_MAX_PROGRAMS, "the large shape holds every program");
+  if (a.P <= 256) hipLaunchKernelGGL((rank_partition_kernel<256, 1>), dim3(1), dim3(256), 0, s, a);
+  else if (a.P <= 1024) hipLaunchKernelGGL((rank_partition_kernel<1024, 1>), dim3(1), dim3(1024), 0, s, a);
+  else hipLaunchKernelGGL((rank_partition_kernel<1024, 4>), dim3(1), dim3(1024), 0, s, a);
   return hipGetLastError();
 }
 
