@@ -219,3 +219,33 @@ def test_default_queue_count_in_order_copies():
                        capture_output=True, text=True, timeout=240)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "smoke ok" in r.stdout
+
+
+@pytest.mark.parametrize("runs_per_half", [1, 2, 3, 7])
+def test_copy_engine_small_staging_many_chunks(runs_per_half):
+    """Copy-engine swaps through a staging buffer of a few runs per half: many
+    chunks per step, programs spanning chunks, both halves reused, and the
+    swap-in's wait for the swap-out falling inside the chunk sequence (a pool
+    with few free pages, so slots land on released pages)."""
+    rng = np.random.default_rng(300 + runs_per_half)
+    geom = Geometry(layers=2, planes=2, block_tokens=2, row_bytes=48, num_blocks=0)
+    run = geom.block_tokens * geom.row_bytes
+    for trial in range(4):
+        inst = random_instance(rng, P=int(rng.integers(4, 24)), max_blocks=9, geom=geom, ties=bool(trial % 2),
+                               tier_p=(0.5, 0.35, 0.15), extra_free=int(rng.integers(0, 4)))
+        if inst.geom.num_blocks == 0:
+            continue
+        log(f"small staging runs/half={runs_per_half} trial={trial} P={inst.P} NB={inst.geom.num_blocks}")
+        pair = Pair(inst, seed=trial, staging_bytes=2 * runs_per_half * run)
+        try:
+            bb = inst.geom.block_bytes
+            recycled = 0
+            for step in range(4):
+                bg = int(rng.integers(inst.geom.num_blocks // 2, inst.geom.num_blocks + 1)) * bb
+                bc = int(rng.integers(0, inst.total_bytes // bb + 2)) * bb
+                w = inst.window if step % 2 == 0 else inst.window[:, :, ::-1].copy()
+                res, plan = pair.step(gpu_bytes=bg, cpu_bytes=bc, window=w, mode=M.MORI_COPY_CE)
+                if plan is not None:
+                    recycled += plan.pages_recycled
+        finally:
+            pair.close()
