@@ -27,15 +27,17 @@ namespace {
 
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 
-// Shape measured on gfx950 with this decode (random 32 KiB pool runs <->
-// contiguous 1 GiB chunks): 256-thread workgroups, one run at a time, eight
-// 16-byte vectors per thread in flight, grid-stride over runs.  Larger
-// workgroups (512, 1024 threads) leave too few workgroups per CU to hide the
-// dependent loads of the per-run decode (-25% at 1024 threads), and handing
-// each workgroup a contiguous block of runs with incremental decode is no
-// faster.
-constexpr int NT = 256;
-constexpr int UNR = 8;
+// Shape measured on gfx950 in the full-size rebalance (32 KiB and 72 KiB
+// runs): 1024-thread workgroups moving one run at a time with two 16-byte
+// vectors per thread in flight (one 32 KiB run per pass), grid-stride over
+// runs.  Against 256 x 8 this is 5% faster for the gather and 8% for the
+// scatter; 512 x 4 lies between, 1024 x 1 and 1024 x 3 match 1024 x 2.  Big
+// workgroups pay off only because the decode is cheap and overlapped: each
+// workgroup walks its programs forward with a cursor instead of searching
+// the program list per run, and decodes the next run before copying the
+// current one, so the dependent page-table load is in flight meanwhile.
+constexpr int NT = 1024;
+constexpr int UNR = 2;
 
 // Largest a in [0, n) with base[a] <= x.
 __device__ inline uint32_t find_slice(const uint32_t* base, uint32_t n, uint64_t x) {
@@ -85,31 +87,49 @@ __device__ inline bool unit_range(const SwapArgs& s, uint32_t n, uint64_t* lo, u
     }
     *hi = (uint64_t)s.pg_base[a] * LC;
   } else if (!kOut && s.part == 2) {
-    if (s.pg_base[n] <= nf) return false;  // no slot reaches a released page
+    if (s.pg_base[n] <= nf) return false;  // no slot reaches a page the swap-out reads
     *lo = (uint64_t)s.pg_base[find_slice(s.pg_base, n, nf)] * LC;
   }
   return *lo < *hi;
 }
 
-// Source and destination of unit u; false when the unit belongs to the other
-// part of a two-part swap-in.
+// Decode state of one workgroup: the moving program of the current unit.  A
+// workgroup's units only increase, so the program index only moves forward.
+struct Cursor {
+  uint32_t a;        // program (index into the direction's list)
+  uint64_t first;    // its first page index / slot
+  uint64_t nb;       // its blocks
+  uint64_t u_first;  // its first unit
+  uint8_t* side;     // its host buffer (direct mode)
+};
+
+__device__ inline void cursor_set(const SwapArgs& s, Cursor& c, uint32_t a) {
+  c.a = a;
+  c.first = s.pg_base[a];
+  c.nb = (uint64_t)s.pg_base[a + 1] - c.first;
+  c.u_first = c.first * s.LC;
+  c.side = s.staging ? nullptr : reinterpret_cast<uint8_t*>(s.addr[s.prog[a]]);
+}
+
+// Source and destination of unit u (u >= the cursor's unit); false when the
+// unit belongs to the other part of a two-part swap-in.
 template <bool kOut>
-__device__ inline bool unit_ends(const SwapArgs& s, uint32_t n, uint64_t u, uint64_t u_lo, const v4u** src,
-                                 v4u** dst) {
-  const uint64_t LC = s.LC;
-  const uint32_t a = find_slice(s.pg_base, n, u / LC);
-  const uint64_t first = s.pg_base[a];
-  const uint64_t nb = (uint64_t)s.pg_base[a + 1] - first;
-  const uint64_t rem = u - first * LC;
-  const uint64_t q = rem / nb, i = rem - q * nb;
-  const uint64_t slot = first + i;
-  if (!kOut && s.part != 0) {
-    const uint64_t nf = s.sum->pages_free_before + s.sum->pages_dropped;
-    if ((s.part == 1) != (slot < nf)) return false;
+__device__ inline bool unit_ends(const SwapArgs& s, uint32_t n, Cursor& c, uint64_t u, uint64_t u_lo, uint64_t nf,
+                                 const v4u** src, v4u** dst) {
+  while (u >= c.u_first + c.nb * s.LC) cursor_set(s, c, c.a + 1);  // never past n - 1 for u < total
+  const uint64_t rem = u - c.u_first;
+  uint64_t q, i;
+  if ((rem >> 32) == 0 && (c.nb >> 32) == 0) {  // the usual case: a 32-bit division
+    q = (uint32_t)rem / (uint32_t)c.nb;
+    i = (uint32_t)rem - (uint32_t)q * (uint32_t)c.nb;
+  } else {
+    q = rem / c.nb;
+    i = rem - q * c.nb;
   }
+  const uint64_t slot = c.first + i;
+  if (!kOut && s.part != 0 && (s.part == 1) != (slot < nf)) return false;
   uint8_t* pool_run = s.pool + (q * s.NB + s.pages[slot]) * s.run;
-  uint8_t* side = s.staging ? s.staging + (u - u_lo) * s.run
-                            : reinterpret_cast<uint8_t*>(s.addr[s.prog[a]]) + rem * s.run;
+  uint8_t* side = s.staging ? s.staging + (u - u_lo) * s.run : c.side + rem * s.run;
   *src = reinterpret_cast<const v4u*>(kOut ? pool_run : side);
   *dst = reinterpret_cast<v4u*>(kOut ? side : pool_run);
   return true;
@@ -121,11 +141,28 @@ __global__ __launch_bounds__(NT) void swap_kernel(SwapArgs s) {
   const uint32_t n = kOut ? s.sum->n_out : s.sum->n_in;
   uint64_t lo, hi;
   if (n == 0 || !unit_range<kOut>(s, n, &lo, &hi)) return;
+  uint64_t u = lo + blockIdx.x;
+  if (u >= hi) return;
   const uint32_t n16 = (uint32_t)(s.run / 16);
-  for (uint64_t u = lo + blockIdx.x; u < hi; u += gridDim.x) {
-    const v4u* src;
-    v4u* dst;
-    if (unit_ends<kOut>(s, n, u, lo, &src, &dst)) copy_run(src, dst, n16, threadIdx.x);
+  const uint64_t nf = s.sum->pages_free_before + s.sum->pages_dropped;
+  Cursor c;
+  cursor_set(s, c, find_slice(s.pg_base, n, u / s.LC));
+  const v4u* src;
+  v4u* dst;
+  bool ok = unit_ends<kOut>(s, n, c, u, lo, nf, &src, &dst);
+  for (;;) {
+    // decode the next unit first: its loads overlap this unit's copy
+    const uint64_t un = u + gridDim.x;
+    const v4u* nsrc = nullptr;
+    v4u* ndst = nullptr;
+    const bool more = un < hi;
+    const bool nok = more && unit_ends<kOut>(s, n, c, un, lo, nf, &nsrc, &ndst);
+    if (ok) copy_run(src, dst, n16, threadIdx.x);
+    if (!more) break;
+    u = un;
+    src = nsrc;
+    dst = ndst;
+    ok = nok;
   }
 }
 
