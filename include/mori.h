@@ -257,8 +257,9 @@ int mori_host_free(void* ptr);
  * slots go to every swapped-in program (from CPU or SSD) in rank order.
  *
  * EINVAL: null pointers (status with MORI_F_STATUS_KEY or MORI_F_INCREMENTAL),
- * P > max_programs, window_k out of range, unknown flags, MORI_F_SSD_TIER with
- * MORI_F_INCREMENTAL, gpu_bytes > num_blocks * block bytes. */
+ * window_k out of range, unknown flags, MORI_F_SSD_TIER with
+ * MORI_F_INCREMENTAL, gpu_bytes > num_blocks * block bytes.  ENOSPC: P above
+ * the context's max_programs.  Both are raised before anything is enqueued. */
 int mori_rank_partition(mori_ctx* ctx, const mori_programs* programs, const mori_budget* budget,
                         void* stream);
 

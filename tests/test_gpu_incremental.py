@@ -102,13 +102,13 @@ def test_max_programs_with_walks(skip_fit):
         pair.close()
 
 
+@pytest.mark.parametrize("P", [256, 700])  # the rank kernel's 256 x 1 and 1024 x 1 shapes
 @pytest.mark.parametrize("mode", MODES)
-def test_phase_changes_and_arrivals(mode):
-    """256 programs over 12 steps: a GPU budget swinging around 55% of the KV,
+def test_phase_changes_and_arrivals(mode, P):
+    """P programs over 12 steps: a GPU budget swinging around 55% of the KV,
     20% of the programs switching between Reasoning and Acting each step, and
     new arrivals joining in Waiting; admitted arrivals become Reasoning."""
-    rng = np.random.default_rng(404 + mode)
-    P = 256
+    rng = np.random.default_rng(404 + mode + P)
     geom = Geometry(layers=2, planes=2, block_tokens=4, row_bytes=64, num_blocks=0)
     inst = random_instance(rng, P=P, max_blocks=24, geom=geom, ties=False, tier_p=(0.5, 0.3, 0.2),
                            extra_free=200)

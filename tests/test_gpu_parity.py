@@ -167,6 +167,10 @@ def test_host_side_state_errors():
                                  window=torch.from_numpy(inst.window).cuda()) == M.MORI_EINVAL
         w = torch.from_numpy(inst.window).cuda()
         assert tp.rank_partition(gpu_bytes=0, cpu_bytes=inst.total_bytes, window=w, flags=64) == M.MORI_EINVAL
+        # more programs than the context was created for: refused before any device access
+        too_many = M.mori_programs(tp.P + 1, w.shape[1], w.data_ptr(), None, None, tp.tbl_off.data_ptr(), tp.tbl_len,
+                                   tp.tbl.data_ptr(), tp.tier.data_ptr(), tp.free_map.data_ptr())
+        assert M.mori_rank_partition(tp.ctx, too_many, M.mori_budget(0, 0, 0, 0), None) == M.MORI_ENOSPC
         assert tp.rank_partition(gpu_bytes=0, cpu_bytes=inst.total_bytes, window=w) == M.MORI_OK
         rc, plan = tp.plan_wait()
         assert rc == 0

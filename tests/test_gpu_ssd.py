@@ -69,6 +69,23 @@ def test_random_instances(seed):
         pair.close()
 
 
+def test_mid_size_program_count():
+    """600 programs (the rank kernel's 1024 x 1 shape) over three tiers, two steps."""
+    rng = np.random.default_rng(600)
+    inst = random_instance(rng, P=600, max_blocks=10, ties=False, tier_p=(0.4, 0.25, 0.15, 0.2), extra_free=50)
+    pair = Pair(inst, seed=6)
+    try:
+        bb = inst.geom.block_bytes
+        nb_total = inst.total_bytes // bb
+        for step in range(2):
+            w = inst.window if step == 0 else inst.window[:, :, ::-1].copy()
+            pair.step(gpu_bytes=int(rng.integers(1, inst.geom.num_blocks + 1)) * bb,
+                      cpu_bytes=int(rng.integers(0, nb_total)) * bb, ssd_bytes=int(rng.integers(0, nb_total)) * bb,
+                      window=w, flags=SSD, mode=MODES[step])
+    finally:
+        pair.close()
+
+
 @pytest.mark.parametrize("mode", MODES)
 def test_tiny_three_tiers(mode):
     """The tiny workload split 40% GPU / 20% CPU / 30% SSD, then the reversed
