@@ -109,6 +109,67 @@ def cpu_baseline(cfg, cpu_frac: float, seconds: float, evict_sizes=(), plan_case
            "sample": (f"{cfg.name} with contexts scaled by {scale:g} ({inst.P} programs, "
                       f"{inst.total_bytes / GIB:.2f} GiB of KV, same GPU/CPU budget fractions), {steps} "
                       f"bidirectional rebalances, memcpy per run between host buffers, single thread")}
+    # the same oracle on all of this process's cores: one thread per core, each
+    # rebalancing its own copy of a smaller sample (the C oracle runs outside
+    # the GIL and its boundary path shares no state between calls)
+    import threading
+
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    small = make_instance(cfg, scale=1.0 / 128)
+    sg = small.geom
+    sbank = make_bank(cfg.seed, cfg.dtype, sg.run_bytes)
+    sbg = budget_bytes(small.total_bytes, cfg.gpu_pct)
+    sbc = int(small.total_bytes * cpu_frac)
+    swins = (small.window, small.window[:, :, ::-1].copy())
+    moved_t = [0] * threads
+    stop = threading.Event()
+
+    errors = []
+
+    def worker(w):
+        try:
+            pool_w = fill_pool_np(small, sbank)
+            bufs_w = [np.zeros(int(n) * sg.block_bytes, np.uint8) for n in small.nblk]
+            tbl_w, tier_w, free_w = small.copy_state()
+            ready.wait(timeout=300)
+            t = 0
+            while not stop.is_set():
+                r = oracle.rebalance(sg, window=swins[t % 2], tbl_off=small.tbl_off, tbl=tbl_w, tier=tier_w,
+                                     free_map=free_w, gpu_budget=sbg, cpu_budget=sbc, pool=pool_w, host_bufs=bufs_w)
+                if t >= 1 and not stop.is_set():
+                    moved_t[w] += r.summary["bytes_out"] + r.summary["bytes_in"]
+                t += 1
+        except Exception as e:  # a failed worker ends the measurement instead of hanging it
+            errors.append(repr(e))
+            ready.abort()
+
+    ready = threading.Barrier(threads + 1)
+    pool_threads = [threading.Thread(target=worker, args=(w,), daemon=True) for w in range(threads)]
+    for th in pool_threads:
+        th.start()
+    try:
+        ready.wait(timeout=300)
+        t0 = time.perf_counter()
+        time.sleep(min(seconds, 8.0))
+    except threading.BrokenBarrierError:
+        t0 = time.perf_counter()
+    stop.set()
+    span = time.perf_counter() - t0
+    for th in pool_threads:
+        th.join()
+    model = ""
+    try:
+        model = next(l.split(":", 1)[1].strip() for l in open("/proc/cpuinfo") if l.startswith("model name"))
+    except (OSError, StopIteration):
+        pass
+    out["value_all_threads"] = None if errors else round(sum(moved_t) / span / 1e9, 3)
+    if errors:
+        out["all_threads_error"] = errors[0]
+    out["threads"] = threads
+    out["cpu_model"] = model
+    out["sample_all_threads"] = (f"{threads} threads, each rebalancing its own copy of {cfg.name} with contexts "
+                                 f"scaled by 1/128 ({small.P} programs, {small.total_bytes / GIB:.2f} GiB of KV) "
+                                 f"for {span:.1f} s; steps still running at the end are not counted")
     # the oracle on the inputs of the eviction-order and rank/partition legs
     out["evict_order_us"] = {}
     for N in evict_sizes:
