@@ -6,7 +6,7 @@
 //            twice, none both owned and free, none out of range, no page held
 //            by a CPU/Waiting program), mark pages of programs leaving the
 //            GPU as released, record the old page of every swap-out block;
-//   count    per 4096-page tile: pages free before the step, released pages
+//   count    per 1024-page tile: pages free before the step, released pages
 //            of dropped programs, released pages of swapped-out programs; a
 //            page that is neither free nor owned is a leak;
 //   scan     one workgroup: exclusive prefix over tiles, totals, capacity;
