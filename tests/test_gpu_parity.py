@@ -253,3 +253,35 @@ def test_copy_engine_small_staging_many_chunks(runs_per_half):
                     recycled += plan.pages_recycled
         finally:
             pair.close()
+
+
+def test_idleness_extreme_windows():
+    """Eq. 1 in binary32 at the edges: denormal times, times near the largest
+    finite value (whose totals stay finite), zeros, exact ties and values whose
+    rounding decides the order -- the device's ranking, prefix and categories
+    equal the oracle's bit for bit (the keys are the idleness bits)."""
+    rng = np.random.default_rng(77)
+    P = 64
+    geom = Geometry(layers=1, planes=1, block_tokens=1, row_bytes=16, num_blocks=0)
+    inst = random_instance(rng, P=P, max_blocks=3, geom=geom, extra_free=8)
+    tiny = np.float32(1.4e-45)          # smallest denormal
+    sub = np.float32(3.0e-39)           # a denormal
+    big = np.float32(3.0e37)            # five of them still sum below the largest finite value
+    vals = np.array([0.0, tiny, sub, 1.0e-30, 0.1, 1.0, 3.0, 1.0e10, big], np.float32)
+    w = vals[rng.integers(0, vals.size, size=(P, 5, 2))].astype(np.float32)
+    w[0] = 0.0                                   # no history: idleness 0
+    w[1, :, 0], w[1, :, 1] = tiny, tiny          # denormal totals: exactly 1/2
+    w[2, :, 0], w[2, :, 1] = 1.0e10, 1.0e-30     # idleness 1e-40: a denormal result
+    w[3, :, 0], w[3, :, 1] = 0.0, sub            # only tool time: 1
+    w[4] = w[5]                                  # an exact tie, broken by id
+    pair = Pair(inst, seed=4)
+    try:
+        bb = inst.geom.block_bytes
+        for bg in (0, inst.geom.num_blocks * bb // 2, inst.geom.num_blocks * bb):
+            res, plan = pair.step(gpu_bytes=bg, cpu_bytes=inst.total_bytes // 2, window=w, mode=M.MORI_COPY_KERNEL)
+            assert res.rc == oracle.OK and plan is not None
+        rc, iota = oracle.idleness(w)
+        assert rc == oracle.OK and iota[1] == np.float32(0.5) and iota[3] == np.float32(1.0) and iota[0] == 0.0
+        assert 0.0 < iota[2] < np.float32(1.2e-38)  # below the smallest normal
+    finally:
+        pair.close()
