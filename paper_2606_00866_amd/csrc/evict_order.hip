@@ -15,7 +15,8 @@
 //   empty launches and no memory traffic)
 //     hist   per tile of keys: 256-bin histogram  -> hist[digit][tile]
 //     dscan  one workgroup per digit: exclusive scan of that digit's counts
-//            over the tiles, and the digit's total
+//            over the tiles, and the digit's total (for at most 16 tiles the
+//            scatter workgroups sum the counts themselves and this launch goes)
 //     scatter per tile: the digit bases (a 256-entry scan of the totals in
 //            LDS) + the tile's scanned count + the stable rank of every key
 //            among the tile's keys of its digit: wave64 ballots over the 8
@@ -193,6 +194,13 @@ __global__ __launch_bounds__(ET) void evict_dscan_kernel(EvictArgs a, int shift)
   if (threadIdx.x == 0) a.dtot[blockIdx.x] = carry;
 }
 
+// Tile counts at or below this are scanned inside each scatter workgroup (its
+// thread d sums digit d over the tiles before its own and over all tiles), so
+// a pass is two launches instead of three.  Measured: at 4 tiles this saves a
+// fifth of the sort; at 69 tiles each thread's strided walk over its row costs
+// more than the launch it saves, so above 16 the separate scan runs.
+constexpr uint32_t INLINE_SCAN_TILES = 16;
+
 template <int EIPT>
 __global__ __launch_bounds__(ET) void evict_scatter_kernel(EvictArgs a, int shift) {
   // s_cnt[slice][wave][digit]: keys of that digit in that wave's 64 keys of the
@@ -208,9 +216,22 @@ __global__ __launch_bounds__(ET) void evict_scatter_kernel(EvictArgs a, int shif
   uint32_t* vd = a.vals[src ^ 1];
   const uint64_t base = (uint64_t)blockIdx.x * (ET * EIPT);
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  uint32_t tot;
-  const uint32_t digit_base = scan256(a.dtot[tid], s_w, &tot);
-  s_off[tid] = digit_base + a.hist[(uint64_t)tid * a.ntiles + blockIdx.x];
+  uint32_t tot, before, total_d;
+  if (a.ntiles <= INLINE_SCAN_TILES) {  // raw counts: sum them here
+    const uint32_t* h = a.hist + (uint64_t)tid * a.ntiles;
+    before = 0;
+    total_d = 0;
+    for (uint32_t t = 0; t < a.ntiles; ++t) {
+      const uint32_t c = h[t];
+      before += t < blockIdx.x ? c : 0u;
+      total_d += c;
+    }
+  } else {  // scanned by evict_dscan_kernel
+    before = a.hist[(uint64_t)tid * a.ntiles + blockIdx.x];
+    total_d = a.dtot[tid];
+  }
+  const uint32_t digit_base = scan256(total_d, s_w, &tot);
+  s_off[tid] = digit_base + before;
 #pragma unroll
   for (int it = 0; it < EIPT; ++it)
 #pragma unroll
@@ -398,7 +419,7 @@ template <int EIPT>
 void launch_tiles(const EvictArgs& a, hipStream_t s) {
   for (int shift = 0; shift < 64; shift += 8) {
     hipLaunchKernelGGL(evict_hist_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a, shift);
-    hipLaunchKernelGGL(evict_dscan_kernel, dim3(256), dim3(ET), 0, s, a, shift);
+    if (a.ntiles > INLINE_SCAN_TILES) hipLaunchKernelGGL(evict_dscan_kernel, dim3(256), dim3(ET), 0, s, a, shift);
     hipLaunchKernelGGL(evict_scatter_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a, shift);
   }
   hipLaunchKernelGGL(evict_prefix_tiles_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a);
