@@ -53,15 +53,16 @@ class Harness:
         del self.tp.pool
         torch.cuda.empty_cache()
 
-    def step(self, window, bg, bc, mode=M.MORI_COPY_AUTO, iota=None):
+    def step(self, window, bg, bc, mode=M.MORI_COPY_AUTO, iota=None, status=None, flags=0):
         inst = self.inst
-        flags = oracle.F_IDLENESS_GIVEN if iota is not None else 0
-        res = oracle.rebalance(self.g, window=window, iota=iota, tbl_off=inst.tbl_off, tbl=self.tbl, tier=self.tier,
-                               free_map=self.free, gpu_budget=bg, cpu_budget=bc, flags=flags)
+        flags |= oracle.F_IDLENESS_GIVEN if iota is not None else 0
+        res = oracle.rebalance(self.g, window=window, iota=iota, status=status, tbl_off=inst.tbl_off, tbl=self.tbl,
+                               tier=self.tier, free_map=self.free, gpu_budget=bg, cpu_budget=bc, flags=flags)
         assert res.rc == oracle.OK
         w = None if window is None else torch.from_numpy(np.ascontiguousarray(window)).cuda()
         it = None if iota is None else torch.from_numpy(np.ascontiguousarray(iota, np.float32)).cuda()
-        plan = self.tp.step(gpu_bytes=bg, cpu_bytes=bc, window=w, idleness=it, flags=flags, mode=mode,
+        st = None if status is None else torch.from_numpy(np.ascontiguousarray(status, np.uint8)).cuda()
+        plan = self.tp.step(gpu_bytes=bg, cpu_bytes=bc, window=w, idleness=it, status=st, flags=flags, mode=mode,
                             s_out=self.s_out, s_in=self.s_in)
         for k in SUMMARY:
             assert getattr(plan, k) == res.summary[k], (self.steps, k, getattr(plan, k), res.summary[k])
@@ -151,6 +152,15 @@ def test_full_size_workload(cfg):
             log(f"  step {t}: out {plan.bytes_out / GIB:.2f} GiB in {plan.bytes_in / GIB:.2f} GiB "
                 f"admit {plan.n_admit_gpu} drop {plan.n_drop_gpu} recycled {plan.pages_recycled}")
         assert plan.n_in > 0 and plan.n_out > 0
+        # the incremental policy (Sec. 4.3.1) at full size: the GPU budget cut by a tenth forces
+        # demotions (Acting first) into CPU room grown by as much; busy programs are Reasoning,
+        # a third of the waiting ones new
+        status = np.where(inst.busy, 0, 1).astype(np.uint8)
+        status[(h.tier == 2) & (np.arange(inst.P) % 3 == 0)] = 2
+        plan = h.step(inst.window, bg - bg // 10, bc + bg // 10, status=status, flags=oracle.F_INCREMENTAL)
+        log(f"  incremental step: out {plan.bytes_out / GIB:.2f} GiB drop {plan.n_drop_gpu} "
+            f"in {plan.n_in} admit {plan.n_admit_gpu}")
+        assert plan.n_out > 0
         h.check_tags()
         log(f"  sampled runs checked: {h.check_bytes()}")
     finally:
