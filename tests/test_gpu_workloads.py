@@ -1,10 +1,12 @@
 """The named workloads on the GPU, in the launch configuration bench.py times
 (copy-engine swaps, 2 GiB of staging per direction in two halves, one pinned CPU-tier arena).
 
-Full-size Llama-3-8B, Llama-3-70B and MLA pools (136-155 GiB of HBM): the oracle
-replays every step's placement and the per-step summaries, final block tables,
-tiers and free map must match exactly; every resident run's tag is checked and
-sampled runs are compared byte for byte with their content-addressed value.
+Full-size Llama-3-8B, Llama-3-70B and MLA pools (136-155 GiB of HBM): three
+boundary-policy steps, one incremental-policy step and one three-tier (SSD)
+step.  The oracle replays every step's placement and the per-step summaries,
+final block tables, tiers and free map must match exactly; every resident
+run's tag is checked and sampled runs are compared byte for byte with their
+content-addressed value.
 
 Churn (1024 programs, 100 steps, GPU budget swinging 45-65%, 10% of programs
 flipping phase per step), scaled to fit one GPU and the pinned-memory ceiling:
@@ -53,17 +55,18 @@ class Harness:
         del self.tp.pool
         torch.cuda.empty_cache()
 
-    def step(self, window, bg, bc, mode=M.MORI_COPY_AUTO, iota=None, status=None, flags=0):
+    def step(self, window, bg, bc, mode=M.MORI_COPY_AUTO, iota=None, status=None, flags=0, ssd=0):
         inst = self.inst
         flags |= oracle.F_IDLENESS_GIVEN if iota is not None else 0
         res = oracle.rebalance(self.g, window=window, iota=iota, status=status, tbl_off=inst.tbl_off, tbl=self.tbl,
-                               tier=self.tier, free_map=self.free, gpu_budget=bg, cpu_budget=bc, flags=flags)
+                               tier=self.tier, free_map=self.free, gpu_budget=bg, cpu_budget=bc, flags=flags,
+                               ssd_budget=ssd)
         assert res.rc == oracle.OK
         w = None if window is None else torch.from_numpy(np.ascontiguousarray(window)).cuda()
         it = None if iota is None else torch.from_numpy(np.ascontiguousarray(iota, np.float32)).cuda()
         st = None if status is None else torch.from_numpy(np.ascontiguousarray(status, np.uint8)).cuda()
         plan = self.tp.step(gpu_bytes=bg, cpu_bytes=bc, window=w, idleness=it, status=st, flags=flags, mode=mode,
-                            s_out=self.s_out, s_in=self.s_in)
+                            s_out=self.s_out, s_in=self.s_in, ssd_bytes=ssd)
         for k in SUMMARY:
             assert getattr(plan, k) == res.summary[k], (self.steps, k, getattr(plan, k), res.summary[k])
         arr = self.tp.plan_arrays(plan)
@@ -89,7 +92,7 @@ class Harness:
             pages = np.concatenate([self.tbl[inst.tbl_off[p]:inst.tbl_off[p + 1]] for p in adm_g]).astype(np.int64)
             fill_pool_torch(self.tp.pool, inst, self.bank_dev, torch.from_numpy(op).cuda(),
                             torch.from_numpy(oi).cuda(), pages=torch.from_numpy(pages).cuda())
-        for p in np.flatnonzero((cat == oracle.ADMIT_CPU) & (inst.nblk > 0)):
+        for p in np.flatnonzero(((cat == oracle.ADMIT_CPU) | (cat == oracle.ADMIT_SSD)) & (inst.nblk > 0)):
             dst = torch.from_numpy(self.tp.host_view(int(p)).view(np.int16))
             dst.copy_(program_content_torch(inst, self.bank_dev, int(p)).cpu())
         torch.cuda.synchronize()
@@ -161,6 +164,10 @@ def test_full_size_workload(cfg):
         log(f"  incremental step: out {plan.bytes_out / GIB:.2f} GiB drop {plan.n_drop_gpu} "
             f"in {plan.n_in} admit {plan.n_admit_gpu}")
         assert plan.n_out > 0
+        # the SSD tier (Sec. 7.1): a third run of the ranking, its KV in host buffers here
+        plan = h.step(inst.window, bg, bc, flags=oracle.F_SSD_TIER, ssd=8 * GIB)
+        log(f"  SSD step: m_ssd {plan.m_ssd} out {plan.n_out} in {plan.n_in}")
+        assert plan.m_ssd > 0
         h.check_tags()
         log(f"  sampled runs checked: {h.check_bytes()}")
     finally:
