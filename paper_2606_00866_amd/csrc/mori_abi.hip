@@ -134,6 +134,19 @@ struct mori_ctx {
     }                                                               \
   } while (0)
 
+// Direct-mode swap launches move their plan's whole direction, whose size the
+// host learns only from that plan; fold it into the profile record before a
+// new plan replaces the host mirror (and when the record is read).
+static int fold_direct_bytes(mori_ctx* c) {
+  if (!c->have_plan || (!c->prof_direct[0] && !c->prof_direct[1])) return MORI_OK;
+  HIP_TRY(c, hipEventSynchronize(c->ev_plan));
+  const DevSummary* s = c->sum_host();
+  c->prof_bytes[0] += c->prof_direct[0] * s->bytes_out;
+  c->prof_bytes[1] += c->prof_direct[1] * s->bytes_in;
+  c->prof_direct[0] = c->prof_direct[1] = 0;
+  return MORI_OK;
+}
+
 static void free_ctx(mori_ctx* c) {
   if (!c) return;
   if (c->ev_plan) (void)hipEventSynchronize(c->ev_plan);
@@ -318,6 +331,7 @@ extern "C" int mori_rank_partition(mori_ctx* ctx, const mori_programs* pr, const
   if (b->gpu_bytes > (uint64_t)ctx->pool.num_blocks * ctx->block_bytes) return MORI_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
   HIP_TRY(ctx, hipSetDevice(ctx->device));
+  if (int rc = fold_direct_bytes(ctx)) return rc;
   if (ctx->out_recorded) HIP_TRY(ctx, hipStreamWaitEvent(s, ctx->ev_out, 0));
   if (ctx->in_recorded) HIP_TRY(ctx, hipStreamWaitEvent(s, ctx->ev_in, 0));
 
@@ -739,17 +753,12 @@ extern "C" int mori_profile_read(mori_ctx* ctx, int direction, uint64_t* launche
     HIP_TRY(ctx, hipEventElapsedTime(&ms, ctx->prof_ev[d][2 * i], ctx->prof_ev[d][2 * i + 1]));
     total += ms;
   }
-  uint64_t bytes = ctx->prof_bytes[d];
-  if (ctx->prof_direct[d] && ctx->have_plan) {
-    HIP_TRY(ctx, hipEventSynchronize(ctx->ev_plan));
-    bytes += ctx->prof_direct[d] * (d ? ctx->sum_host()->bytes_in : ctx->sum_host()->bytes_out);
-  }
+  if (int rc = fold_direct_bytes(ctx)) return rc;
   *launches = ctx->prof_n[d];
-  *payload_bytes = bytes;
+  *payload_bytes = ctx->prof_bytes[d];
   *kernel_ms = total;
   ctx->prof_n[d] = 0;
   ctx->prof_bytes[d] = 0;
-  ctx->prof_direct[d] = 0;
   return MORI_OK;
 }
 

@@ -285,3 +285,36 @@ def test_idleness_extreme_windows():
         assert 0.0 < iota[2] < np.float32(1.2e-38)  # below the smallest normal
     finally:
         pair.close()
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_profile_counters(mode):
+    """mori_profile / mori_profile_read: launches, payload bytes (each plan's own
+    bytes, also when several plans run between reads) and time per direction;
+    a read clears the record; nothing is recorded while profiling is off."""
+    rng = np.random.default_rng(55)
+    geom = Geometry(layers=2, planes=2, block_tokens=2, row_bytes=48, num_blocks=0)
+    inst = random_instance(rng, P=16, max_blocks=8, geom=geom, tier_p=(0.5, 0.4, 0.1), extra_free=6)
+    run = geom.block_tokens * geom.row_bytes
+    pair = Pair(inst, seed=5, staging_bytes=2 * 3 * run)  # three runs per half: several chunks per step
+    try:
+        ctx, bb = pair.tp.ctx, inst.geom.block_bytes
+        assert M.mori_profile(ctx, True) == M.MORI_OK
+        moved = [0, 0]
+        for step in range(3):
+            w = inst.window if step % 2 == 0 else inst.window[:, :, ::-1].copy()
+            bg = int(rng.integers(inst.geom.num_blocks // 3, inst.geom.num_blocks + 1)) * bb
+            res, plan = pair.step(gpu_bytes=bg, cpu_bytes=inst.total_bytes, window=w, mode=mode)
+            moved[0] += plan.bytes_out
+            moved[1] += plan.bytes_in
+        assert moved[0] > 0 and moved[1] > 0
+        for d in (0, 1):
+            rc, n, by, ms = M.mori_profile_read(ctx, d)
+            assert rc == M.MORI_OK and by == moved[d] and n > 0 and ms > 0.0
+            assert M.mori_profile_read(ctx, d)[1:] == (0, 0, 0.0)  # cleared
+        assert M.mori_profile(ctx, False) == M.MORI_OK
+        pair.step(gpu_bytes=0, cpu_bytes=inst.total_bytes, window=inst.window, mode=mode)
+        assert M.mori_profile_read(ctx, 0)[1] == 0
+        assert M.mori_profile_read(ctx, 2)[0] == M.MORI_EINVAL
+    finally:
+        pair.close()
