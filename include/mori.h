@@ -256,6 +256,11 @@ int mori_host_free(void* ptr);
  * coming back is swapped in from a host buffer the caller has filled; page
  * slots go to every swapped-in program (from CPU or SSD) in rank order.
  *
+ * A new plan supersedes the last one.  It waits (on the stream) for the last
+ * plan's swaps that were enqueued; swaps that were not are abandoned, and the
+ * tables, tiers and free map stand as that plan wrote them -- programs it sent
+ * off the GPU then have no copy of their KV (placement-only use).
+ *
  * EINVAL: null pointers (status with MORI_F_STATUS_KEY or MORI_F_INCREMENTAL),
  * window_k out of range, unknown flags, MORI_F_SSD_TIER with
  * MORI_F_INCREMENTAL, gpu_bytes > num_blocks * block bytes.  ENOSPC: P above

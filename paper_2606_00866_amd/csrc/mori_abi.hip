@@ -147,21 +147,35 @@ static int fold_direct_bytes(mori_ctx* c) {
   return MORI_OK;
 }
 
+static void destroy_profile_events(mori_ctx* c) {
+  for (int d = 0; d < 2; ++d) {
+    for (hipEvent_t e : c->prof_ev[d])
+      if (e) {
+        (void)hipEventSynchronize(e);
+        (void)hipEventDestroy(e);
+      }
+    c->prof_ev[d].clear();
+    c->prof_n[d] = 0;
+  }
+}
+
 static void free_ctx(mori_ctx* c) {
   if (!c) return;
+  // everything the context enqueued has finished before its memory goes
   if (c->ev_plan) (void)hipEventSynchronize(c->ev_plan);
   if (c->ev_out) (void)hipEventSynchronize(c->ev_out);
   if (c->ev_in) (void)hipEventSynchronize(c->ev_in);
   for (int d = 0; d < 2; ++d)
     if (c->ev_addr[d]) (void)hipEventSynchronize(c->ev_addr[d]);
+  for (int d = 0; d < 2; ++d)
+    if (c->cstream[d]) (void)hipStreamSynchronize(c->cstream[d]);
+  destroy_profile_events(c);
   if (c->blob_dev) (void)hipFree(c->blob_dev);
   if (c->scratch) (void)hipFree(c->scratch);
   for (int d = 0; d < 2; ++d)
     if (c->staging[d]) (void)hipFree(c->staging[d]);
   if (c->blob_host) (void)hipHostFree(c->blob_host);
   if (c->addr_pinned) (void)hipHostFree(c->addr_pinned);
-  for (int d = 0; d < 2; ++d)
-    if (c->cstream[d]) (void)hipStreamSynchronize(c->cstream[d]);
   hipEvent_t evs[] = {c->ev_plan,          c->ev_out,           c->ev_in,           c->ev_addr[0],
                       c->ev_addr[1],       c->ev_start[0],      c->ev_start[1],     c->ev_half_ready[0][0],
                       c->ev_half_ready[0][1], c->ev_half_ready[1][0], c->ev_half_ready[1][1],
@@ -170,11 +184,6 @@ static void free_ctx(mori_ctx* c) {
     if (e) (void)hipEventDestroy(e);
   for (int d = 0; d < 2; ++d)
     if (c->cstream[d]) (void)hipStreamDestroy(c->cstream[d]);
-  for (int d = 0; d < 2; ++d)
-    for (hipEvent_t e : c->prof_ev[d]) {
-      (void)hipEventSynchronize(e);
-      (void)hipEventDestroy(e);
-    }
   delete c;
 }
 
@@ -288,9 +297,11 @@ extern "C" int mori_register(mori_ctx* ctx, void* ptr, uint64_t bytes) {
   const uint64_t d1 = reinterpret_cast<uint64_t>(a1.devicePointer);
   if (d1 - d0 != bytes - 1) return MORI_EINVAL;  // one contiguous mapping
   DevRange r{reinterpret_cast<uint64_t>(ptr), bytes, d0, device ? 1ull : 0ull};
+  // the new entry goes to the device first, then to the host list, so a
+  // failure registers nothing; entries a swap may be reading are not written
+  HIP_TRY(ctx, hipSetDevice(ctx->device));
+  HIP_TRY(ctx, hipMemcpy(ctx->ranges_dev + ctx->ranges.size(), &r, sizeof r, hipMemcpyHostToDevice));
   ctx->ranges.push_back(r);
-  HIP_TRY(ctx, hipMemcpy(ctx->ranges_dev, ctx->ranges.data(), sizeof(DevRange) * ctx->ranges.size(),
-                         hipMemcpyHostToDevice));
   return MORI_OK;
 }
 
@@ -334,6 +345,8 @@ extern "C" int mori_rank_partition(mori_ctx* ctx, const mori_programs* pr, const
   if (int rc = fold_direct_bytes(ctx)) return rc;
   if (ctx->out_recorded) HIP_TRY(ctx, hipStreamWaitEvent(s, ctx->ev_out, 0));
   if (ctx->in_recorded) HIP_TRY(ctx, hipStreamWaitEvent(s, ctx->ev_in, 0));
+  // from here the previous plan is superseded: a launch that fails leaves none
+  ctx->have_plan = false;
 
   PlanArgs a{};
   a.window = pr->window;
@@ -733,9 +746,19 @@ extern "C" int mori_evict_order(const mori_blocks* b, uint32_t tier, uint64_t ne
 extern "C" int mori_profile(mori_ctx* ctx, int enable) {
   if (!ctx) return MORI_EINVAL;
   if (enable && ctx->prof_ev[0].empty()) {
+    HIP_TRY(ctx, hipSetDevice(ctx->device));
     for (int d = 0; d < 2; ++d) {
       ctx->prof_ev[d].resize(2 * mori_ctx::kProfCap, nullptr);
-      for (hipEvent_t& e : ctx->prof_ev[d]) HIP_TRY(ctx, hipEventCreate(&e));
+      for (hipEvent_t& e : ctx->prof_ev[d]) {
+        const hipError_t err = hipEventCreate(&e);
+        if (err != hipSuccess) {
+          e = nullptr;
+          ctx->last_hip_error = (int)err;
+          (void)hipGetLastError();
+          destroy_profile_events(ctx);
+          return MORI_EHIP;
+        }
+      }
     }
   }
   ctx->profiling = enable != 0;

@@ -8,7 +8,7 @@ import torch
 from gpu_helpers import Pair, log
 from oracle import oracle
 from paper_2606_00866_amd import mori as M
-from paper_2606_00866_amd.tiering import MoriError
+from paper_2606_00866_amd.tiering import MoriError, TierPool
 from workload import TINY, Geometry, budget_bytes, make_instance, random_instance
 
 pytestmark = pytest.mark.gpu
@@ -318,3 +318,100 @@ def test_profile_counters(mode):
         assert M.mori_profile_read(ctx, 2)[0] == M.MORI_EINVAL
     finally:
         pair.close()
+
+
+@pytest.mark.parametrize("where,mode", [("device", M.MORI_COPY_AUTO), ("two_ranges", M.MORI_COPY_KERNEL),
+                                        ("two_ranges", M.MORI_COPY_CE)])
+def test_buffers_in_other_registered_ranges(where, mode):
+    """CPU-tier buffers in a registered device-memory range (AUTO then resolves
+    to the kernels at the device grid) or alternating between two pinned host
+    ranges registered beside the pool's arena: tables, tiers, free map, resident
+    pages and every buffer byte equal the oracle's over three steps; then the
+    range limit (ENOSPC) and unknown memory (EINVAL)."""
+    import ctypes
+
+    from workload import fill_pool_np, make_bank, program_host_content
+
+    rng = np.random.default_rng(77)
+    geom = Geometry(layers=2, planes=2, block_tokens=4, row_bytes=64, num_blocks=0)
+    inst = random_instance(rng, P=24, max_blocks=10, geom=geom, tier_p=(0.55, 0.45), extra_free=8)
+    g, bb = inst.geom, inst.geom.block_bytes
+    bank = make_bank(3, inst.dtype, g.run_bytes)
+    pool = fill_pool_np(inst, bank)
+    bufs = [program_host_content(inst, bank, p).copy() if inst.tier[p] == 1
+            else np.zeros(int(inst.nblk[p]) * bb, np.uint8) for p in range(inst.P)]
+    extent = [(-(-int(n) * bb // 256)) * 256 for n in inst.nblk]
+    off = np.concatenate([[0], np.cumsum(extent)]).astype(np.int64)
+    tbl, tier, free = inst.copy_state()
+    tp = TierPool(g, inst.tbl_off, inst.tbl, inst.tier, inst.free_map, arena_bytes=4096)
+    hosts = []
+    try:
+        tp.pool.copy_(torch.from_numpy(pool).cuda())
+        if where == "device":
+            dbuf = torch.zeros(int(off[-1]) + 256, dtype=torch.uint8, device="cuda")
+            assert M.mori_register(tp.ctx, dbuf.data_ptr(), dbuf.numel()) == M.MORI_OK
+            addr = np.array([dbuf.data_ptr() + o for o in off[:-1]], np.uint64)
+            read = lambda p: dbuf[off[p]:off[p] + bufs[p].size].cpu().numpy()
+            for p in range(inst.P):
+                if bufs[p].size:
+                    dbuf[off[p]:off[p] + bufs[p].size] = torch.from_numpy(bufs[p]).cuda()
+        else:
+            for _ in range(2):
+                rc, h = M.mori_host_alloc(int(off[-1]) + 256)
+                assert rc == M.MORI_OK
+                hosts.append(h)
+                assert M.mori_register(tp.ctx, h, int(off[-1]) + 256) == M.MORI_OK
+            addr = np.array([hosts[p % 2] + o for p, o in enumerate(off[:-1])], np.uint64)
+            view = lambda p: np.ctypeslib.as_array((ctypes.c_uint8 * bufs[p].size).from_address(int(addr[p])))
+            read = lambda p: view(p).copy()
+            for p in range(inst.P):
+                if bufs[p].size:
+                    view(p)[:] = bufs[p]
+        s_out, s_in = torch.cuda.Stream(), torch.cuda.Stream()
+        for t in range(3):
+            w = inst.window if t != 1 else inst.window[:, :, ::-1].copy()
+            bg = int(rng.integers(g.num_blocks // 4, g.num_blocks + 1)) * bb
+            res = oracle.rebalance(g, window=w, tbl_off=inst.tbl_off, tbl=tbl, tier=tier, free_map=free,
+                                   gpu_budget=bg, cpu_budget=inst.total_bytes, pool=pool, host_bufs=bufs)
+            assert res.rc == oracle.OK
+            assert tp.rank_partition(gpu_bytes=bg, cpu_bytes=inst.total_bytes,
+                                     window=torch.from_numpy(np.ascontiguousarray(w)).cuda(), stream=s_out) == 0
+            rc, plan = tp.plan_wait()
+            assert rc == M.MORI_OK
+            assert M.mori_kv_swap_out(tp.ctx, addr.ctypes.data, mode, s_out.cuda_stream) == M.MORI_OK
+            assert M.mori_kv_swap_in(tp.ctx, addr.ctypes.data, mode, s_in.cuda_stream) == M.MORI_OK
+            torch.cuda.synchronize()
+            assert M.mori_query(tp.ctx, M.MORI_Q_DEVICE_ERROR) == (M.MORI_OK, 0)
+            used = M.mori_query(tp.ctx, M.MORI_Q_LAST_MODE)[1]
+            assert used == (M.MORI_COPY_KERNEL if where == "device" else mode)
+            log(f"  {where} step {t}: out {plan.n_out} in {plan.n_in} mode {used}")
+            t_, r_, f_ = tp.state()
+            assert (t_ == tbl).all() and (r_ == tier).all() and (f_ == free).all()
+            dpool = tp.pool.cpu().numpy().reshape(g.nplanes, g.num_blocks, g.run_bytes)
+            owned = tbl[tbl != 0xFFFFFFFF].astype(np.int64)
+            assert np.array_equal(dpool[:, owned], pool.reshape(g.nplanes, g.num_blocks, g.run_bytes)[:, owned])
+            for p in np.flatnonzero(tier == 1):
+                assert np.array_equal(read(p), bufs[p]), p
+        # the context holds MORI_MAX_RANGES ranges (the pool's arena is one)
+        extra = []
+        while True:
+            rc, h = M.mori_host_alloc(4096)
+            assert rc == M.MORI_OK
+            extra.append(h)
+            rc = M.mori_register(tp.ctx, h, 4096)
+            if rc != M.MORI_OK:
+                break
+        assert rc == M.MORI_ENOSPC and 1 + len(hosts) + (where == "device") + len(extra) - 1 == M.MORI_MAX_RANGES
+        hosts += extra
+        junk = np.zeros(4096, np.uint8)
+        tp2 = TierPool(g, inst.tbl_off, inst.tbl, inst.tier, inst.free_map, arena_bytes=4096)
+        try:
+            assert M.mori_register(tp2.ctx, junk.ctypes.data, junk.size) == M.MORI_EINVAL  # pageable memory
+            assert M.mori_register(tp2.ctx, hosts[0], 0) == M.MORI_EINVAL
+        finally:
+            tp2.close()
+    finally:
+        torch.cuda.synchronize()
+        tp.close()
+        for h in hosts:
+            M.mori_host_free(h)
