@@ -272,6 +272,14 @@ def measure_peaks(torch, M, s1, s2):
                        "rate of the other, its tail after the first ended taken at its one-direction rate)")}
 
 
+def link_bound_s(out_bytes: int, in_bytes: int, peaks: dict) -> float:
+    """Lower bound on the time of one step's D2H and H2D bytes on the measured
+    link: neither direction beats its one-direction rate and both together do
+    not beat the two-way capacity."""
+    return max(out_bytes / (peaks["d2h_GBps"] * 1e9), in_bytes / (peaks["h2d_GBps"] * 1e9),
+               (out_bytes + in_bytes) / (peaks["bidir_GBps"] * 1e9))
+
+
 def evict_inputs(np, N):
     """Synthetic block metadata of the eviction-order leg (Sec. 4.3.2): N
     blocks of 1024 programs, half the timestamps tied, variable block sizes,
@@ -520,6 +528,7 @@ def main() -> int:
     prof = [M.mori_profile_read(tp.ctx, d) for d in (0, 1)]
     M.mori_profile(tp.ctx, False)
     value = moved / elapsed / 1e9
+    mix_bound_s = sum(link_bound_s(h["bytes_out"], h["bytes_in"], peaks) for h in history[-args.steps:])
     log(f"timed {args.steps} steps: {moved / GIB:.2f} GiB in {elapsed:.3f} s -> {value:.2f} GB/s")
 
     # dominant kernel: the gather/scatter kernel of the direction on the step's
@@ -575,7 +584,11 @@ def main() -> int:
             "cpu_budget_bytes": bc,
             "bytes_per_step": int(moved / max(args.steps, 1)),
         },
-        "hostlink": {**peaks, "frac_of_bidir_peak": round(value / peaks["bidir_GBps"], 4)},
+        "hostlink": {**peaks, "frac_of_bidir_peak": round(value / peaks["bidir_GBps"], 4),
+                     "frac_of_mix_bound": round(mix_bound_s / elapsed, 4),
+                     "mix_bound": ("lower bound on the timed steps' time on this link, per step max(out / d2h, "
+                                   "in / h2d, (out + in) / bidir), summed; frac_of_mix_bound = that bound over the "
+                                   "measured time (equals frac_of_bidir_peak when every step moves as much each way)")},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": stored_traffic(cfg.name, crit),
                      "algorithmic_bytes_per_launch": int(2 * dom["payload_bytes"] / max(dom["launches"], 1)),

@@ -8,6 +8,7 @@ here they are first-fit extents inside one pinned, device-mapped arena.
 """
 from __future__ import annotations
 
+import bisect
 import ctypes as C
 from dataclasses import dataclass
 
@@ -48,14 +49,18 @@ class FirstFit:
         return None
 
     def release(self, off: int) -> None:
+        """Returns an extent, merged with free neighbours (free list kept sorted
+        by offset: a binary search and at most two merges)."""
         size = self.used.pop(off)
-        merged = []
-        for s, n in sorted(self.free + [(off, size)]):
-            if merged and merged[-1][0] + merged[-1][1] == s:
-                merged[-1] = (merged[-1][0], merged[-1][1] + n)
-            else:
-                merged.append((s, n))
-        self.free = merged
+        i = bisect.bisect_left(self.free, (off, 0))
+        if i > 0 and self.free[i - 1][0] + self.free[i - 1][1] == off:
+            i -= 1
+            off, size = self.free[i][0], self.free[i][1] + size
+            del self.free[i]
+        if i < len(self.free) and off + size == self.free[i][0]:
+            size += self.free[i][1]
+            del self.free[i]
+        self.free.insert(i, (off, size))
 
     @property
     def bytes_used(self) -> int:
