@@ -194,50 +194,76 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     return;
   }
 
-  // ---- 2. stable LSD radix sort of (key, id), 4-bit digits ---------------
-  // Digit counters are laid out (digit, it, wave) so an exclusive scan over
-  // them in thread order gives every (digit, item slice, wave) its output base
-  // in (digit, original position) order, i.e. a stable pass.  Digits on which
-  // every real key agrees are skipped; padding keeps the tail.
-  const uint64_t varying = s_or ^ s_and;
-  const uint64_t lanemask_lt = (1ull << lane) - 1ull;
-  for (int shift = 0; shift < KEY_BITS; shift += RADIX_BITS) {
-    if (((varying >> shift) & (RADIX - 1)) == 0) continue;
-    uint32_t digit[IPT], lrank[IPT];
-    s_cnt[tid] = 0;
+  // ---- 2. stable sort of (key, id) ---------------------------------------
+  if constexpr (IPT == 1 && RT <= 256) {
+    // P <= 256: each program's rank is the number of programs before it in
+    // (key, id) order, counted against every key in LDS (the same address for
+    // all lanes, a broadcast): P steps and four barriers, where the radix sort
+    // takes up to sixteen passes of several barriers and a workgroup scan each.
+    s_key[tid] = key[0];
     __syncthreads();
-#pragma unroll
-    for (int it = 0; it < IPT; ++it) {
-      const uint32_t d = (uint32_t)(key[it] >> shift) & (RADIX - 1);
-      uint64_t same = ~0ull;
-#pragma unroll
-      for (int b = 0; b < RADIX_BITS; ++b) {
-        const uint64_t bal = __ballot((d >> b) & 1u);
-        same &= ((d >> b) & 1u) ? bal : ~bal;
+    uint32_t rank = tid;  // padding keeps its slot: every real rank is below P
+    if ((uint32_t)tid < P) {
+      const uint64_t k = key[0];
+      rank = 0;
+      for (uint32_t j = 0; j < P; ++j) {
+        const uint64_t kj = s_key[j];
+        rank += (kj < k) | ((kj == k) & (j < (uint32_t)tid));
       }
-      const uint32_t r = __popcll(same & lanemask_lt);
-      if (r == 0) s_cnt[(d * IPT + it) * NW + wid] = __popcll(same);
-      digit[it] = d;
-      lrank[it] = r;
     }
     __syncthreads();
-    uint32_t tot;
-    const uint32_t base = block_scan_excl<NW, uint32_t>(s_cnt[tid], s_w32, &tot);
-    s_cnt[tid] = base;
+    s_key[rank] = key[0];
+    s_id[rank] = id[0];
     __syncthreads();
+    key[0] = s_key[tid];
+    id[0] = s_id[tid];
+    __syncthreads();
+  } else {
+    // LSD radix sort, 4-bit digits.  Digit counters are laid out (digit, it,
+    // wave) so an exclusive scan over them in thread order gives every (digit,
+    // item slice, wave) its output base in (digit, original position) order,
+    // i.e. a stable pass.  Digits on which every real key agrees are skipped;
+    // padding keeps the tail.
+    const uint64_t varying = s_or ^ s_and;
+    const uint64_t lanemask_lt = (1ull << lane) - 1ull;
+    for (int shift = 0; shift < KEY_BITS; shift += RADIX_BITS) {
+      if (((varying >> shift) & (RADIX - 1)) == 0) continue;
+      uint32_t digit[IPT], lrank[IPT];
+      s_cnt[tid] = 0;
+      __syncthreads();
 #pragma unroll
-    for (int it = 0; it < IPT; ++it) {
-      const uint32_t pos = s_cnt[(digit[it] * IPT + it) * NW + wid] + lrank[it];
-      s_key[pos] = key[it];
-      s_id[pos] = id[it];
-    }
-    __syncthreads();
+      for (int it = 0; it < IPT; ++it) {
+        const uint32_t d = (uint32_t)(key[it] >> shift) & (RADIX - 1);
+        uint64_t same = ~0ull;
 #pragma unroll
-    for (int it = 0; it < IPT; ++it) {
-      key[it] = s_key[it * RT + tid];
-      id[it] = s_id[it * RT + tid];
+        for (int b = 0; b < RADIX_BITS; ++b) {
+          const uint64_t bal = __ballot((d >> b) & 1u);
+          same &= ((d >> b) & 1u) ? bal : ~bal;
+        }
+        const uint32_t r = __popcll(same & lanemask_lt);
+        if (r == 0) s_cnt[(d * IPT + it) * NW + wid] = __popcll(same);
+        digit[it] = d;
+        lrank[it] = r;
+      }
+      __syncthreads();
+      uint32_t tot;
+      const uint32_t base = block_scan_excl<NW, uint32_t>(s_cnt[tid], s_w32, &tot);
+      s_cnt[tid] = base;
+      __syncthreads();
+#pragma unroll
+      for (int it = 0; it < IPT; ++it) {
+        const uint32_t pos = s_cnt[(digit[it] * IPT + it) * NW + wid] + lrank[it];
+        s_key[pos] = key[it];
+        s_id[pos] = id[it];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int it = 0; it < IPT; ++it) {
+        key[it] = s_key[it * RT + tid];
+        id[it] = s_id[it * RT + tid];
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
   // item x now holds rank x: id[it] is the program at rank it * RT + tid
   uint32_t nb[IPT];
