@@ -31,7 +31,7 @@ namespace {
 // (barriers over 4 waves), 1024 x 1 up to 1024 and 1024 threads x 4 items
 // (striped: item x = it * RT + tid) up to 4096; fewer item slices mean fewer
 // workgroup scans, which dominate this latency-bound step.
-constexpr int RADIX_BITS = 4;
+constexpr int RADIX_BITS = 8;
 constexpr int RADIX = 1 << RADIX_BITS;
 constexpr int KEY_BITS = 64;
 constexpr int GROUP_SHIFT = 61;  // incremental keys: listing group in the top three bits
@@ -66,6 +66,56 @@ __device__ T block_scan_excl(T v, T* s_wave, T* total) {
   return res;
 }
 
+// Exclusive scans of the IPT x RT items in rank order (item it of thread tid
+// has rank it * RT + tid), N values per item side by side: wave scans, the
+// per-(slice, wave) totals scanned by the first wave, and three barriers in
+// all, however many slices.  s_tot needs (IPT * NW + 1) * N entries; total[n]
+// receives the sum of value n over all items.
+template <int NW, int IPT, int N>
+__device__ void scan_slices(const uint64_t (&v)[IPT][N], uint64_t (&ex)[IPT][N], uint64_t* s_tot,
+                            uint64_t (&total)[N]) {
+  constexpr int NS = IPT * NW;
+  static_assert(NS <= 64, "one lane per (slice, wave) total");
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  uint64_t inc[IPT][N];
+#pragma unroll
+  for (int it = 0; it < IPT; ++it)
+#pragma unroll
+    for (int n = 0; n < N; ++n) {
+      uint64_t x = v[it][n];
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint64_t y = __shfl_up(x, off, 64);
+        if (lane >= off) x += y;
+      }
+      inc[it][n] = x;
+      if (lane == 63) s_tot[(it * NW + wid) * N + n] = x;
+    }
+  __syncthreads();
+  if (wid == 0) {
+#pragma unroll
+    for (int n = 0; n < N; ++n) {
+      const uint64_t w = lane < NS ? s_tot[lane * N + n] : 0ull;
+      uint64_t wi = w;
+#pragma unroll
+      for (int off = 1; off < NS; off <<= 1) {
+        const uint64_t y = __shfl_up(wi, off, 64);
+        if (lane >= off) wi += y;
+      }
+      if (lane < NS) s_tot[lane * N + n] = wi - w;
+      if (lane == NS - 1) s_tot[NS * N + n] = wi;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int it = 0; it < IPT; ++it)
+#pragma unroll
+    for (int n = 0; n < N; ++n) ex[it][n] = s_tot[(it * NW + wid) * N + n] + inc[it][n] - v[it][n];
+#pragma unroll
+  for (int n = 0; n < N; ++n) total[n] = s_tot[NS * N + n];
+  __syncthreads();
+}
+
 // Transition category.  Leaving the GPU for a tier that keeps the KV (CPU,
 // SSD) is a swap-out, the reverse a swap-in.
 __device__ inline uint8_t category(uint8_t from, uint8_t to) {
@@ -84,12 +134,19 @@ __device__ inline uint8_t category(uint8_t from, uint8_t to) {
 template <int RT, int IPT>
 __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
   constexpr int NW = RT / 64;  // wavefronts
-  static_assert(RADIX * IPT * NW <= RT, "one digit counter per thread");
+  constexpr int NCNT = RADIX * IPT * NW;  // digit counters, (digit, item slice, wave)
+  constexpr int CPT = NCNT / RT;         // consecutive counters per thread in their scan
+  static_assert(NCNT % RT == 0, "whole counters per thread");
+  // counter c lives at c + c / 32: a thread's CPT consecutive counters then
+  // fall in different banks from its neighbours'
+  auto cidx = [](uint32_t c) { return c + (c >> 5); };
   __shared__ uint64_t s_key[RT * IPT];  // sort scratch, then the inclusive byte prefix by rank
   __shared__ uint32_t s_id[RT * IPT];   // sort scratch, then blocks by rank
-  __shared__ uint32_t s_cnt[RT];
+  __shared__ uint32_t s_cnt[NCNT + NCNT / 32];
   __shared__ uint8_t s_tier[RT * IPT];
-  __shared__ uint64_t s_w64[NW + 1];
+  __shared__ uint32_t s_nblk[RT * IPT];  // blocks of program x
+  __shared__ uint8_t s_told[RT * IPT];   // old tier of program x
+  __shared__ uint64_t s_tot[(IPT * NW + 1) * 2];
   __shared__ uint32_t s_w32[NW + 1];
   __shared__ unsigned long long s_or, s_and;
   __shared__ uint32_t s_err, s_m_gpu, s_m_cpu, s_m_ssd;
@@ -112,10 +169,6 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     s_n_drop_gpu = s_n_drop_cpu = s_n_admit_gpu = s_n_admit_cpu = 0;
     s_gpu_after = s_cpu_after = s_ssd_after = 0;
     s_gpu_part = s_upper_part = 0;
-    DevSummary z = {};
-    z.num_programs = P;
-    *a.sum = z;
-    *a.swap_err = 0;
   }
   __syncthreads();
 
@@ -138,6 +191,8 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     const uint32_t off0 = a.tbl_off[x], off1 = a.tbl_off[x + 1];
     if (told > top_tier) err |= MORI_DEV_BAD_TIER;
     if (off1 < off0) err |= MORI_DEV_BAD_TBL_OFF;
+    s_nblk[x] = off1 - off0;
+    s_told[x] = told;
     float v;
     if (a.flags & MORI_F_IDLENESS_GIVEN) {
       v = a.idleness[x];
@@ -145,11 +200,24 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     } else {
       float t_reasoning = 0.0f, t_acting = 0.0f;
       const float* w = a.window + (size_t)x * a.k * 2;
-      for (uint32_t j = 0; j < a.k; ++j) {
-        const float r = w[2 * j], c = w[2 * j + 1];
-        if (!(r >= 0.0f) || !(c >= 0.0f) || __builtin_isinf(r) || __builtin_isinf(c)) err |= MORI_DEV_BAD_WINDOW;
-        t_reasoning = t_reasoning + r;
-        t_acting = t_acting + c;
+      for (uint32_t j0 = 0; j0 < a.k; j0 += 8) {  // eight cycles' loads in flight, then the sums in order
+        float rv[8], cv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          rv[u] = cv[u] = 0.0f;
+          if (j0 + u < a.k) {
+            rv[u] = w[2 * (j0 + u)];
+            cv[u] = w[2 * (j0 + u) + 1];
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (j0 + u >= a.k) break;
+          const float r = rv[u], c = cv[u];
+          if (!(r >= 0.0f) || !(c >= 0.0f) || __builtin_isinf(r) || __builtin_isinf(c)) err |= MORI_DEV_BAD_WINDOW;
+          t_reasoning = t_reasoning + r;
+          t_acting = t_acting + c;
+        }
       }
       const float total = t_reasoning + t_acting;
       if (__builtin_isinf(t_reasoning) || __builtin_isinf(t_acting) || __builtin_isinf(total))
@@ -190,7 +258,13 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
   if (err) atomicOr(&s_err, err);
   __syncthreads();
   if (s_err) {
-    if (tid == 0) atomicOr(&a.sum->error, s_err);
+    if (tid == 0) {
+      DevSummary z = {};
+      z.num_programs = P;
+      z.error = s_err;
+      *a.sum = z;
+      *a.swap_err = 0;
+    }
     return;
   }
 
@@ -219,17 +293,18 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     id[0] = s_id[tid];
     __syncthreads();
   } else {
-    // LSD radix sort, 4-bit digits.  Digit counters are laid out (digit, it,
-    // wave) so an exclusive scan over them in thread order gives every (digit,
-    // item slice, wave) its output base in (digit, original position) order,
-    // i.e. a stable pass.  Digits on which every real key agrees are skipped;
-    // padding keeps the tail.
+    // LSD radix sort, 8-bit digits (at most four passes over idleness keys).
+    // Digit counters are laid out (digit, it, wave) so an exclusive scan over
+    // them in index order gives every (digit, item slice, wave) its output
+    // base in (digit, original position) order, i.e. a stable pass.  Digits
+    // on which every real key agrees are skipped; padding keeps the tail.
     const uint64_t varying = s_or ^ s_and;
     const uint64_t lanemask_lt = (1ull << lane) - 1ull;
     for (int shift = 0; shift < KEY_BITS; shift += RADIX_BITS) {
       if (((varying >> shift) & (RADIX - 1)) == 0) continue;
       uint32_t digit[IPT], lrank[IPT];
-      s_cnt[tid] = 0;
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) s_cnt[cidx(j * RT + tid)] = 0;
       __syncthreads();
 #pragma unroll
       for (int it = 0; it < IPT; ++it) {
@@ -241,18 +316,27 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
           same &= ((d >> b) & 1u) ? bal : ~bal;
         }
         const uint32_t r = __popcll(same & lanemask_lt);
-        if (r == 0) s_cnt[(d * IPT + it) * NW + wid] = __popcll(same);
+        if (r == 0) s_cnt[cidx((d * IPT + it) * NW + wid)] = __popcll(same);
         digit[it] = d;
         lrank[it] = r;
       }
       __syncthreads();
-      uint32_t tot;
-      const uint32_t base = block_scan_excl<NW, uint32_t>(s_cnt[tid], s_w32, &tot);
-      s_cnt[tid] = base;
+      uint32_t loc[CPT], sum = 0, tot;
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) {
+        loc[j] = s_cnt[cidx(tid * CPT + j)];
+        sum += loc[j];
+      }
+      uint32_t base = block_scan_excl<NW, uint32_t>(sum, s_w32, &tot);
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) {
+        s_cnt[cidx(tid * CPT + j)] = base;
+        base += loc[j];
+      }
       __syncthreads();
 #pragma unroll
       for (int it = 0; it < IPT; ++it) {
-        const uint32_t pos = s_cnt[(digit[it] * IPT + it) * NW + wid] + lrank[it];
+        const uint32_t pos = s_cnt[cidx((digit[it] * IPT + it) * NW + wid)] + lrank[it];
         s_key[pos] = key[it];
         s_id[pos] = id[it];
       }
@@ -271,26 +355,24 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
   for (int it = 0; it < IPT; ++it) {
     const uint32_t r = it * RT + tid;
     nb[it] = 0;
-    if (r < P) {
-      a.order[r] = id[it];
-      nb[it] = a.tbl_off[id[it] + 1] - a.tbl_off[id[it]];
-    }
-    s_id[r] = nb[it];
+    if (r < P) nb[it] = s_nblk[id[it]];
   }
+  __syncthreads();  // s_id is reused for blocks by rank
+#pragma unroll
+  for (int it = 0; it < IPT; ++it) s_id[it * RT + tid] = nb[it];
 
   // ---- 3. KV-byte prefix in that order and the placement ----------------
   uint64_t S[IPT];
-  uint64_t carry = 0;
+  {
+    uint64_t bytes[IPT][1], ex[IPT][1], tot[1];
 #pragma unroll
-  for (int it = 0; it < IPT; ++it) {
-    const uint64_t bytes = (uint64_t)nb[it] * a.block_bytes;
-    uint64_t tot;
-    const uint64_t ex = block_scan_excl<NW, uint64_t>(bytes, s_w64, &tot);
-    S[it] = carry + ex + bytes;
-    carry += tot;
-    const uint32_t r = it * RT + tid;
-    s_key[r] = S[it];
-    if (r < P) a.prefix[r] = S[it];
+    for (int it = 0; it < IPT; ++it) bytes[it][0] = (uint64_t)nb[it] * a.block_bytes;
+    scan_slices<NW, IPT, 1>(bytes, ex, s_tot, tot);
+#pragma unroll
+    for (int it = 0; it < IPT; ++it) {
+      S[it] = ex[it][0] + bytes[it][0];
+      s_key[it * RT + tid] = S[it];
+    }
   }
   if (incremental) {
     // listing groups: [0, g1) GPU, [g1, g2) CPU, [g2, g3) Waiting returning,
@@ -338,17 +420,18 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     }
     // (3) promotion: a strict prefix of the candidates' byte scan
     if (!(a.flags & MORI_F_SKIP_FIT)) {
-      uint64_t ccarry = 0;
+      uint64_t cb[IPT][1], ex[IPT][1], tot[1];
+      bool cand[IPT];
 #pragma unroll
       for (int it = 0; it < IPT; ++it) {
         const uint32_t r = it * RT + tid;
-        const bool cand = (r >= g1 && r < c_end) || (r >= g2 && r < g4);
-        const uint64_t cb = cand ? (uint64_t)nb[it] * a.block_bytes : 0;
-        uint64_t tot;
-        const uint64_t T = ccarry + block_scan_excl<NW, uint64_t>(cb, s_w64, &tot) + cb;
-        ccarry += tot;
-        if (cand && T <= room_gpu) s_tier[r] = MORI_TIER_GPU;
+        cand[it] = (r >= g1 && r < c_end) || (r >= g2 && r < g4);
+        cb[it][0] = cand[it] ? (uint64_t)nb[it] * a.block_bytes : 0;
       }
+      scan_slices<NW, IPT, 1>(cb, ex, s_tot, tot);
+#pragma unroll
+      for (int it = 0; it < IPT; ++it)
+        if (cand[it] && ex[it][0] + cb[it][0] <= room_gpu) s_tier[it * RT + tid] = MORI_TIER_GPU;
     }
     __syncthreads();
     if (tid == 0) {
@@ -470,9 +553,10 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
 
   // ---- 4. sticky diff: categories, lists in rank order, bases -----------
   // packed scans: A = pages_out | pages_in << 32, B = pages_admit | n_out << 32 | n_in << 48
-  uint64_t exA[IPT], exB[IPT];
-  uint8_t catv[IPT];
-  uint64_t carryA = 0, carryB = 0;
+  // Global stores wait until after the last barrier: a barrier waits for the
+  // stores still in flight, so stores issued earlier would stall every one.
+  uint64_t vab[IPT][2], exab[IPT][2], totab[2];
+  uint8_t catv[IPT], toldv[IPT], tnewv[IPT];
   uint32_t n_dg = 0, n_dc = 0, n_ag = 0, n_ac = 0;
   uint64_t gpu_after = 0, cpu_after = 0, ssd_after = 0;
 #pragma unroll
@@ -482,12 +566,11 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     catv[it] = MORI_CAT_KEPT;
     if (r < P) {
       const uint32_t p = id[it];
-      const uint8_t told = a.tier[p], tnew = s_tier[r];
+      const uint8_t told = s_told[p], tnew = s_tier[r];
       const uint8_t c = category(told, tnew);
       catv[it] = c;
-      a.tier_old[p] = told;
-      a.tier_new[p] = tnew;
-      a.cat[p] = c;
+      toldv[it] = told;
+      tnewv[it] = tnew;
       if (c == MORI_CAT_OUT) va = nb[it], vb = 1ull << 32;
       if (c == MORI_CAT_IN) va = (uint64_t)nb[it] << 32, vb = 1ull << 48;
       if (c == MORI_CAT_ADMIT_GPU) vb = nb[it], ++n_ag;
@@ -498,23 +581,38 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
       if (tnew == MORI_TIER_CPU) cpu_after += (uint64_t)nb[it] * a.block_bytes;
       if (tnew == MORI_TIER_SSD) ssd_after += (uint64_t)nb[it] * a.block_bytes;
     }
-    uint64_t tA, tB;
-    exA[it] = carryA + block_scan_excl<NW, uint64_t>(va, s_w64, &tA);
-    exB[it] = carryB + block_scan_excl<NW, uint64_t>(vb, s_w64, &tB);
-    carryA += tA;
-    carryB += tB;
+    vab[it][0] = va;
+    vab[it][1] = vb;
   }
+  scan_slices<NW, IPT, 2>(vab, exab, s_tot, totab);
+  const uint64_t carryA = totab[0], carryB = totab[1];
   const uint32_t pages_out = (uint32_t)(carryA & 0xFFFFFFFFu), pages_in = (uint32_t)(carryA >> 32);
   const uint32_t pages_admit = (uint32_t)(carryB & 0xFFFFFFFFu);
   const uint32_t n_out = (uint32_t)((carryB >> 32) & 0xFFFFu), n_in = (uint32_t)(carryB >> 48);
+  if (n_dg) atomicAdd(&s_n_drop_gpu, n_dg);
+  if (n_dc) atomicAdd(&s_n_drop_cpu, n_dc);
+  if (n_ag) atomicAdd(&s_n_admit_gpu, n_ag);
+  if (n_ac) atomicAdd(&s_n_admit_cpu, n_ac);
+  if (gpu_after) atomicAdd(&s_gpu_after, (unsigned long long)gpu_after);
+  if (cpu_after) atomicAdd(&s_cpu_after, (unsigned long long)cpu_after);
+  if (ssd_after) atomicAdd(&s_ssd_after, (unsigned long long)ssd_after);
+  __syncthreads();
+
+  // ---- 5. the plan's stores ------------------------------------------------
 #pragma unroll
   for (int it = 0; it < IPT; ++it) {
     const uint32_t r = it * RT + tid;
     if (r >= P) continue;
     const uint32_t p = id[it];
-    const uint32_t pg_out_ex = (uint32_t)(exA[it] & 0xFFFFFFFFu), pg_in_ex = (uint32_t)(exA[it] >> 32);
-    const uint32_t pg_admit_ex = (uint32_t)(exB[it] & 0xFFFFFFFFu);
-    const uint32_t idx_out = (uint32_t)((exB[it] >> 32) & 0xFFFFu), idx_in = (uint32_t)(exB[it] >> 48);
+    a.order[r] = p;
+    a.prefix[r] = S[it];
+    a.tier_old[p] = toldv[it];
+    a.tier_new[p] = tnewv[it];
+    a.cat[p] = catv[it];
+    const uint64_t exA = exab[it][0], exB = exab[it][1];
+    const uint32_t pg_out_ex = (uint32_t)(exA & 0xFFFFFFFFu), pg_in_ex = (uint32_t)(exA >> 32);
+    const uint32_t pg_admit_ex = (uint32_t)(exB & 0xFFFFFFFFu);
+    const uint32_t idx_out = (uint32_t)((exB >> 32) & 0xFFFFu), idx_in = (uint32_t)(exB >> 48);
     switch (catv[it]) {
       case MORI_CAT_OUT:
         a.out_prog[idx_out] = p;
@@ -533,36 +631,31 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
         break;
     }
   }
-  if (n_dg) atomicAdd(&s_n_drop_gpu, n_dg);
-  if (n_dc) atomicAdd(&s_n_drop_cpu, n_dc);
-  if (n_ag) atomicAdd(&s_n_admit_gpu, n_ag);
-  if (n_ac) atomicAdd(&s_n_admit_cpu, n_ac);
-  if (gpu_after) atomicAdd(&s_gpu_after, (unsigned long long)gpu_after);
-  if (cpu_after) atomicAdd(&s_cpu_after, (unsigned long long)cpu_after);
-  if (ssd_after) atomicAdd(&s_ssd_after, (unsigned long long)ssd_after);
-  __syncthreads();
   if (tid == 0) {
     a.out_pg_base[n_out] = pages_out;
     a.in_pg_base[n_in] = pages_in;
-    DevSummary* s = a.sum;
-    s->m_gpu = s_m_gpu;
-    s->m_cpu = s_m_cpu;
-    s->m_ssd = s_m_ssd;
-    s->n_out = n_out;
-    s->n_in = n_in;
-    s->n_drop_gpu = s_n_drop_gpu;
-    s->n_drop_cpu = s_n_drop_cpu;
-    s->n_admit_gpu = s_n_admit_gpu;
-    s->n_admit_cpu = s_n_admit_cpu;
-    s->pages_out = pages_out;
-    s->pages_in = pages_in;
-    s->pages_admit = pages_admit;
-    s->bytes_out = (uint64_t)pages_out * a.block_bytes;
-    s->bytes_in = (uint64_t)pages_in * a.block_bytes;
-    s->gpu_bytes_after = s_gpu_after;
-    s->cpu_bytes_after = s_cpu_after;
-    s->ssd_bytes_after = s_ssd_after;
-    s->need = (uint64_t)pages_in + pages_admit;
+    DevSummary z = {};  // the page fields follow in the page kernels
+    z.num_programs = P;
+    z.m_gpu = s_m_gpu;
+    z.m_cpu = s_m_cpu;
+    z.m_ssd = s_m_ssd;
+    z.n_out = n_out;
+    z.n_in = n_in;
+    z.n_drop_gpu = s_n_drop_gpu;
+    z.n_drop_cpu = s_n_drop_cpu;
+    z.n_admit_gpu = s_n_admit_gpu;
+    z.n_admit_cpu = s_n_admit_cpu;
+    z.pages_out = pages_out;
+    z.pages_in = pages_in;
+    z.pages_admit = pages_admit;
+    z.bytes_out = (uint64_t)pages_out * a.block_bytes;
+    z.bytes_in = (uint64_t)pages_in * a.block_bytes;
+    z.gpu_bytes_after = s_gpu_after;
+    z.cpu_bytes_after = s_cpu_after;
+    z.ssd_bytes_after = s_ssd_after;
+    z.need = (uint64_t)pages_in + pages_admit;
+    *a.sum = z;
+    *a.swap_err = 0;
   }
 }
 
