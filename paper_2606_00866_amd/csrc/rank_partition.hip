@@ -2,8 +2,9 @@
 //
 //   1. idleness of every program by Eq. 1 (Sec. 4.2), binary32, totals
 //      accumulated oldest cycle first from +0, correctly rounded division;
-//   2. a 64-bit key per program and a stable LSD radix sort of (key, id) with
-//      wave64 ballots.  Boundary policy: the key is the idleness bits,
+//   2. a 64-bit key per program and a stable sort of (key, id): direct rank
+//      counting for up to 256 programs, else an LSD radix sort with wave64
+//      ballots.  Boundary policy: the key is the idleness bits,
 //      optionally with the Acting bit of the demotion order of Sec. 4.3.1 --
 //      the relative ranking, busiest first.  Incremental policy (Sec. 4.3.1):
 //      the key is the program's listing group (old tier; Waiting split into
@@ -28,9 +29,9 @@ namespace mori {
 namespace {
 
 // Three shapes, chosen by P at launch: 256 threads x 1 item for P <= 256
-// (barriers over 4 waves), 1024 x 1 up to 1024 and 1024 threads x 4 items
-// (striped: item x = it * RT + tid) up to 4096; fewer item slices mean fewer
-// workgroup scans, which dominate this latency-bound step.
+// (barriers over 4 waves; ranks counted directly), 1024 x 1 up to 1024 and
+// 1024 threads x 4 items (striped: item x = it * RT + tid) up to 4096; fewer
+// item slices mean fewer ballots and digit counters per radix pass.
 constexpr int RADIX_BITS = 8;
 constexpr int RADIX = 1 << RADIX_BITS;
 constexpr int KEY_BITS = 64;
