@@ -415,3 +415,24 @@ def test_buffers_in_other_registered_ranges(where, mode):
         tp.close()
         for h in hosts:
             M.mori_host_free(h)
+
+
+def test_two_contexts_interleaved():
+    """Two pools, each with its own context and streams, rebalanced in turn:
+    contexts share nothing, so each matches its own oracle run."""
+    rng = np.random.default_rng(31)
+    geom = Geometry(layers=2, planes=2, block_tokens=2, row_bytes=64, num_blocks=0)
+    insts = [random_instance(rng, P=int(rng.integers(20, 60)), max_blocks=10, geom=geom, tier_p=(0.5, 0.35, 0.15),
+                             extra_free=int(rng.integers(2, 20))) for _ in range(2)]
+    pairs = [Pair(inst, seed=40 + i) for i, inst in enumerate(insts)]
+    try:
+        for step in range(4):
+            for i, (inst, pair) in enumerate(zip(insts, pairs)):
+                bb = inst.geom.block_bytes
+                bg = int(rng.integers(inst.geom.num_blocks // 3, inst.geom.num_blocks + 1)) * bb
+                w = inst.window if (step + i) % 2 == 0 else inst.window[:, :, ::-1].copy()
+                log(f"context {i} step {step} P={inst.P} NB={inst.geom.num_blocks}")
+                pair.step(gpu_bytes=bg, cpu_bytes=inst.total_bytes, window=w, mode=MODES[(step + i) % 2])
+    finally:
+        for pair in pairs:
+            pair.close()
