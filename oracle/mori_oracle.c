@@ -201,11 +201,11 @@ static uint32_t orc_promote_level(const uint8_t* status, const uint8_t* tier_old
   return status[p] == ORC_ST_NEW ? 2 : 1;
 }
 
-/* comparison context for qsort (single-threaded oracle) */
-static const float* orc_sort_iota;
-static const uint8_t* orc_sort_status;
-static const uint8_t* orc_sort_tier;
-static const uint32_t* orc_sort_nblk;
+/* comparison context for qsort, one per thread so concurrent calls are safe */
+static _Thread_local const float* orc_sort_iota;
+static _Thread_local const uint8_t* orc_sort_status;
+static _Thread_local const uint8_t* orc_sort_tier;
+static _Thread_local const uint32_t* orc_sort_nblk;
 
 static int orc_promote_cmp(const void* a, const void* b) {
   uint32_t x = *(const uint32_t*)a, y = *(const uint32_t*)b;

@@ -232,3 +232,44 @@ def test_rejects_bad_input(orc):
                         free_map=np.ones(1, np.uint8), gpu_budget=16, cpu_budget=0,
                         flags=orc.F_IDLENESS_GIVEN | orc.F_INCREMENTAL)
     assert res.rc == orc.E_INPUT
+
+
+def test_concurrent_calls_match_sequential(orc):
+    """The oracle's sort context is per thread: incremental placements run on
+    eight threads at once (the C call releases the GIL) give the results of the
+    same calls run one after another."""
+    import threading
+
+    rng = np.random.default_rng(808)
+    cases = []
+    for _ in range(16):
+        P = int(rng.integers(50, 400))
+        iota = rng.choice(np.array([0.0, 0.25, 0.5, 0.75, 1.0], np.float32), P)  # ties exercise the comparators
+        status = rng.integers(0, 3, P).astype(np.uint8)
+        tier = rng.integers(0, 3, P).astype(np.uint8)
+        nblk = rng.integers(0, 30, P).astype(np.uint32)
+        total = int(nblk.sum())
+        cases.append((iota, status, tier, nblk, int(rng.integers(0, total + 1)), int(rng.integers(0, total + 1))))
+    expect = [orc.incremental(i, s, t, n, 1, g, c) for i, s, t, n, g, c in cases]
+    got, errors = {}, []
+
+    def work(k):
+        try:
+            for rep in range(20):
+                j = (k + rep) % len(cases)
+                i, s, t, n, g, c = cases[j]
+                got.setdefault(j, []).append(orc.incremental(i, s, t, n, 1, g, c))
+        except Exception as e:  # pragma: no cover - reported below
+            errors.append(e)
+
+    threads = [threading.Thread(target=work, args=(k,)) for k in range(8)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    assert not errors
+    for j, runs in got.items():
+        for r in runs:
+            assert r[0] == expect[j][0] and r[4:] == expect[j][4:]
+            for a, b in zip(r[1:4], expect[j][1:4]):
+                assert np.array_equal(a, b)
