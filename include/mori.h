@@ -212,7 +212,8 @@ int mori_host_free(void* ptr);
 
 /* Computes the new placement and rewrites tbl, tier and free_map in stream
  * order.  Waits (on the stream) for the previous plan's swaps.  The plan is
- * copied to the context's pinned mirror; read it with mori_plan_wait.
+ * stored into the context's pinned host mirror by the kernels; read it with
+ * mori_plan_wait.
  *
  * Pages for programs entering the GPU are handed out in this order: pages
  * free before the step, then pages of programs dropped to Waiting (nothing

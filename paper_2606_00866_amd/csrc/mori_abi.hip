@@ -2,8 +2,8 @@
 // pinned plan mirror, staging), stream/event ordering of the three calls, and
 // the two copy modes of the swaps.
 //
-//   plan       rank kernel -> page kernels -> async copy of the plan blob to
-//              the pinned mirror -> plan event.
+//   plan       rank kernel (and the page state) -> page kernels, which also
+//              store the plan into its pinned host mirror -> plan event.
 //   swap-out   direct: translate addresses -> gather kernel storing straight
 //              into host-mapped memory; copy engine: per chunk, gather kernel
 //              into one half of a device staging buffer (caller's stream) ->
@@ -82,6 +82,7 @@ struct mori_ctx {
   BlobLayout L{};
   uint8_t* blob_dev = nullptr;   // plan blob on the device
   uint8_t* blob_host = nullptr;  // pinned mirror
+  uint8_t* blob_host_dev = nullptr;  // the mirror as the device addresses it
   uint8_t* scratch = nullptr;    // device-only arrays
   uint32_t* base = nullptr;
   uint32_t* pstate = nullptr;
@@ -222,8 +223,10 @@ extern "C" int mori_create(const mori_pool* pool, uint32_t max_programs, uint64_
   hipError_t e;
   if ((e = hipGetDevice(&c->device)) != hipSuccess) return fail(e);
   if ((e = hipMalloc(&c->blob_dev, c->L.total)) != hipSuccess) return fail(e);
-  if ((e = hipHostMalloc(&c->blob_host, c->L.total, hipHostMallocDefault)) != hipSuccess) return fail(e);
+  if ((e = hipHostMalloc(&c->blob_host, c->L.total, hipHostMallocMapped)) != hipSuccess) return fail(e);
   std::memset(c->blob_host, 0, c->L.total);
+  if ((e = hipHostGetDevicePointer(reinterpret_cast<void**>(&c->blob_host_dev), c->blob_host, 0)) != hipSuccess)
+    return fail(e);
   // device-only scratch, 256-B aligned pieces
   const uint64_t NB = pool->num_blocks, pm = max_programs;
   size_t o = 0;
@@ -383,9 +386,9 @@ extern "C" int mori_rank_partition(mori_ctx* ctx, const mori_programs* pr, const
   a.tile_cnt = ctx->tile_cnt;
   a.tile_base = ctx->tile_base;
   a.swap_err = ctx->swap_err;
+  a.host_delta = reinterpret_cast<int64_t>(ctx->blob_host_dev) - reinterpret_cast<int64_t>(ctx->blob_dev);
   HIP_TRY(ctx, launch_rank(a, s));
   HIP_TRY(ctx, launch_pages(a, s));
-  HIP_TRY(ctx, hipMemcpyAsync(ctx->blob_host, ctx->blob_dev, ctx->L.total, hipMemcpyDeviceToHost, s));
   HIP_TRY(ctx, hipEventRecord(ctx->ev_plan, s));
   ctx->have_plan = true;
   ctx->out_enqueued = ctx->in_enqueued = false;

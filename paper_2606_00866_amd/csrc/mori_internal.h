@@ -17,7 +17,7 @@ constexpr uint32_t PS_COPY = 8u;   // ... whose KV the swap-out reads from it fi
 constexpr int PAGE_TILE = 1024;    // pages per workgroup in the page-allocation kernels (4 per thread)
 constexpr int PAGE_WG = 256;       // threads per page-allocation workgroup (16 pages each)
 
-// Plan summary as kept on the device (the head of the plan blob copied to the host).
+// Plan summary as kept on the device (the head of the plan blob, mirrored on the host).
 struct DevSummary {
   uint32_t num_programs, m_gpu, m_cpu, m_ssd;
   uint32_t n_out, n_in, n_drop_gpu, n_drop_cpu, n_admit_gpu, n_admit_cpu;
@@ -68,7 +68,16 @@ struct PlanArgs {
   uint64_t* tile_cnt;     // [2 ntiles]: packed (free-before, dropped << 32), then swapped-out counts
   uint64_t* tile_base;    // [2 ntiles] exclusive prefixes of both halves of tile_cnt
   uint32_t* swap_err;     // cleared by every plan
+  // The pinned host mirror of the plan blob, as the device addresses it: the
+  // kernels that finish a part of the plan store it there too, so no copy of
+  // the blob follows the plan.  Mirror address = blob address + host_delta.
+  int64_t host_delta;
 };
+
+template <typename T>
+__device__ inline T* host_mirror(const PlanArgs& a, T* blob_ptr) {
+  return reinterpret_cast<T*>(reinterpret_cast<char*>(blob_ptr) + a.host_delta);
+}
 
 // Everything a swap kernel reads.
 struct SwapArgs {

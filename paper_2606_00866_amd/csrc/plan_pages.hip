@@ -1,7 +1,7 @@
 // Page side of one rebalance (sticky placement of Sec. 4.3 over the paged KV
-// pool of Sec. 2.1), after the rank / boundary kernel:
+// pool of Sec. 2.1), after the rank / boundary kernel (whose other workgroups
+// set the page state from the caller's free map):
 //
-//   init     page state from the caller's free map;
 //   claim    walk every block-table entry: validate ownership (no page owned
 //            twice, none both owned and free, none out of range, no page held
 //            by a CPU/Waiting program), mark pages of programs leaving the
@@ -10,6 +10,7 @@
 //            of dropped programs, released pages of swapped-out programs; a
 //            page that is neither free nor owned is a leak;
 //   scan     one workgroup: exclusive prefix over tiles, totals, capacity;
+//            the summary is final here and is stored into the host mirror;
 //   assign   slot j of the incoming programs takes the j-th page of
 //            (free-before ++ dropped ++ swapped out, each ascending): pages
 //            nothing reads come before pages the swap-out reads, so the
@@ -38,12 +39,6 @@ __device__ inline uint32_t find_program(const uint32_t* off, uint32_t P, uint32_
     else hi = mid;
   }
   return lo;
-}
-
-__global__ __launch_bounds__(WG) void pages_init_kernel(PlanArgs a) {
-  if (a.sum->error) return;
-  for (uint32_t pg = blockIdx.x * WG + threadIdx.x; pg < a.NB; pg += gridDim.x * WG)
-    a.pstate[pg] = a.free_map[pg] ? PS_FREE : 0u;
 }
 
 __global__ __launch_bounds__(WG) void pages_claim_kernel(PlanArgs a) {
@@ -136,7 +131,10 @@ __device__ uint64_t wg_scan_excl(uint64_t v, uint64_t* s_wave, uint64_t* total) 
 
 __global__ __launch_bounds__(1024) void pages_scan_kernel(PlanArgs a) {
   __shared__ uint64_t s_wave[1024 / 64 + 1];
-  if (a.sum->error) return;
+  if (a.sum->error) {
+    if (threadIdx.x == 0) *host_mirror(a, a.sum) = *a.sum;
+    return;
+  }
   uint64_t carry[2] = {0, 0};
   for (int half = 0; half < 2; ++half) {  // (free-before | dropped << 32), then swapped out
     const uint64_t* cnt = a.tile_cnt + (uint64_t)half * a.ntiles;
@@ -162,6 +160,7 @@ __global__ __launch_bounds__(1024) void pages_scan_kernel(PlanArgs a) {
       s->pages_recycled = s->need > nf ? s->need - nf : 0;
       s->pages_free_after = nf + nd + nc - s->need;
     }
+    *host_mirror(a, s) = *s;  // the summary is final from here
   }
 }
 
@@ -257,8 +256,7 @@ inline uint32_t grid_for(uint64_t n, uint32_t cap) {
 }  // namespace
 
 hipError_t launch_pages(const PlanArgs& a, hipStream_t s) {
-  const uint32_t gp = grid_for(a.NB, 2048), ge = grid_for(a.tbl_len > a.P ? a.tbl_len : a.P, 2048);
-  hipLaunchKernelGGL(pages_init_kernel, dim3(gp), dim3(WG), 0, s, a);
+  const uint32_t ge = grid_for(a.tbl_len > a.P ? a.tbl_len : a.P, 2048);
   hipLaunchKernelGGL(pages_claim_kernel, dim3(ge), dim3(WG), 0, s, a);
   if (a.ntiles) hipLaunchKernelGGL(pages_count_kernel, dim3(a.ntiles), dim3(WG), 0, s, a);
   hipLaunchKernelGGL(pages_scan_kernel, dim3(1), dim3(1024), 0, s, a);

@@ -156,6 +156,14 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
   __shared__ unsigned long long s_gpu_after, s_cpu_after, s_ssd_after, s_gpu_part, s_upper_part;
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  if (blockIdx.x > 0) {
+    // the other workgroups set up the page state for the page kernels (it
+    // depends on the caller's free map only)
+    const uint64_t stride = (uint64_t)(gridDim.x - 1) * RT;
+    for (uint64_t pg = (uint64_t)(blockIdx.x - 1) * RT + tid; pg < a.NB; pg += stride)
+      a.pstate[pg] = a.free_map[pg] ? PS_FREE : 0u;
+    return;
+  }
   const uint32_t P = a.P;
   const bool incremental = (a.flags & MORI_F_INCREMENTAL) != 0;
   const bool ssd = (a.flags & MORI_F_SSD_TIER) != 0;
@@ -264,6 +272,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
       z.num_programs = P;
       z.error = s_err;
       *a.sum = z;
+      *host_mirror(a, a.sum) = z;
       *a.swap_err = 0;
     }
     return;
@@ -610,6 +619,11 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     a.tier_old[p] = toldv[it];
     a.tier_new[p] = tnewv[it];
     a.cat[p] = catv[it];
+    *host_mirror(a, a.order + r) = p;
+    *host_mirror(a, a.prefix + r) = S[it];
+    *host_mirror(a, a.tier_old + p) = toldv[it];
+    *host_mirror(a, a.tier_new + p) = tnewv[it];
+    *host_mirror(a, a.cat + p) = catv[it];
     const uint64_t exA = exab[it][0], exB = exab[it][1];
     const uint32_t pg_out_ex = (uint32_t)(exA & 0xFFFFFFFFu), pg_in_ex = (uint32_t)(exA >> 32);
     const uint32_t pg_admit_ex = (uint32_t)(exB & 0xFFFFFFFFu);
@@ -618,11 +632,15 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
       case MORI_CAT_OUT:
         a.out_prog[idx_out] = p;
         a.out_pg_base[idx_out] = pg_out_ex;
+        *host_mirror(a, a.out_prog + idx_out) = p;
+        *host_mirror(a, a.out_pg_base + idx_out) = pg_out_ex;
         a.base[p] = pg_out_ex;
         break;
       case MORI_CAT_IN:  // programs promoted from the CPU (or SSD) tier take the first slots (Sec. 4.3.1)
         a.in_prog[idx_in] = p;
         a.in_pg_base[idx_in] = pg_in_ex;
+        *host_mirror(a, a.in_prog + idx_in) = p;
+        *host_mirror(a, a.in_pg_base + idx_in) = pg_in_ex;
         a.base[p] = pg_in_ex;
         break;
       case MORI_CAT_ADMIT_GPU:  // then programs admitted from Waiting (priority (2))
@@ -635,7 +653,9 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
   if (tid == 0) {
     a.out_pg_base[n_out] = pages_out;
     a.in_pg_base[n_in] = pages_in;
-    DevSummary z = {};  // the page fields follow in the page kernels
+    *host_mirror(a, a.out_pg_base + n_out) = pages_out;
+    *host_mirror(a, a.in_pg_base + n_in) = pages_in;
+    DevSummary z = {};  // the page fields follow in the page kernels, which mirror the summary
     z.num_programs = P;
     z.m_gpu = s_m_gpu;
     z.m_cpu = s_m_cpu;
@@ -664,9 +684,14 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
 
 hipError_t launch_rank(const PlanArgs& a, hipStream_t s) {
   static_assert(1024 * 4 == (int)MORI_MAX_PROGRAMS, "the large shape holds every program");
-  if (a.P <= 256) hipLaunchKernelGGL((rank_partition_kernel<256, 1>), dim3(1), dim3(256), 0, s, a);
-  else if (a.P <= 1024) hipLaunchKernelGGL((rank_partition_kernel<1024, 1>), dim3(1), dim3(1024), 0, s, a);
-  else hipLaunchKernelGGL((rank_partition_kernel<1024, 4>), dim3(1), dim3(1024), 0, s, a);
+  // workgroup 0 ranks; the others (about four pages per thread) set up the page state
+  auto grid = [&](uint32_t rt) {
+    const uint64_t g = ((uint64_t)a.NB + 4ull * rt - 1) / (4ull * rt);
+    return dim3(1 + (uint32_t)(g < 1024 ? g : 1024));
+  };
+  if (a.P <= 256) hipLaunchKernelGGL((rank_partition_kernel<256, 1>), grid(256), dim3(256), 0, s, a);
+  else if (a.P <= 1024) hipLaunchKernelGGL((rank_partition_kernel<1024, 1>), grid(1024), dim3(1024), 0, s, a);
+  else hipLaunchKernelGGL((rank_partition_kernel<1024, 4>), grid(1024), dim3(1024), 0, s, a);
   return hipGetLastError();
 }
 
