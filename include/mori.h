@@ -76,6 +76,8 @@ extern "C" {
 #define MORI_DEV_HOST_ADDR 0x200u     /* swap address not 16-B aligned or outside registered memory */
 #define MORI_DEV_BAD_BLOCK 0x400u     /* eviction order: type label > 2 or last access >= 2^62 */
 #define MORI_DEV_BAD_STATUS 0x800u    /* incremental policy: status value > 2 */
+#define MORI_DEV_STALL 0x1000u        /* eviction order: a sort pass waited too long on another
+                                         workgroup (not expected; the result is not valid) */
 /* classes: program data = 0x00F and 0x800, pool state = 0x0F0, capacity = 0x100, swap = 0x200,
    blocks = 0x400 */
 

@@ -8,21 +8,36 @@
 // 64-bit key (type position << 62 | last access) with the block id riding
 // along, done here as a device-wide stable LSD radix sort:
 //
-//   keys     build keys, validate, OR/AND of all keys;
+//   keys     build keys, validate, OR/AND of all keys; for the one-kernel
+//            passes also the digit counts of all eight passes at once (they
+//            do not depend on the order), one set per workgroup, equal keys
+//            (the blocks of a program share their time) counted once per run;
+//   totals   those counts summed over the keys workgroups;
 //   per pass (8-bit digit, 8 passes; a digit on which every key agrees needs
 //   no pass, and each kernel works out from the OR/AND which of the two
-//   key/value buffers holds the current order, so such a pass costs three
-//   empty launches and no memory traffic)
-//     hist   per tile of keys: 256-bin histogram  -> hist[digit][tile]
-//     dscan  one workgroup per digit: exclusive scan of that digit's counts
-//            over the tiles, and the digit's total (for at most 16 tiles the
-//            scatter workgroups sum the counts themselves and this launch goes)
-//     scatter per tile: the digit bases (a 256-entry scan of the totals in
-//            LDS) + the tile's scanned count + the stable rank of every key
-//            among the tile's keys of its digit: wave64 ballots over the 8
-//            digit bits rank each key within its wave's 64 keys of a slice,
-//            one scan per digit over (slice, wave) in LDS orders the groups as
-//            the keys were ordered -> position (two barriers per tile);
+//   key/value buffers holds the current order, so such a pass is empty
+//   launches and no memory traffic), one workgroup per tile, in one of two
+//   forms by tile count:
+//     one kernel (up to ONESWEEP_TILES tiles):
+//     - the tile index comes from a counter in the order workgroups start, so
+//       every lower tile belongs to a workgroup that is already running;
+//     - the stable rank of every key among the tile's keys of its digit:
+//       wave64 ballots over the 8 digit bits rank it within its wave's 64
+//       keys of a slice, one scan per digit over (slice, wave) in LDS orders
+//       the groups as the keys were ordered;
+//     - the tile's count of each digit is published, then the keys of that
+//       digit in all lower tiles are summed by looking back over the
+//       published counts, eight tiles per round, until a tile that already
+//       holds its inclusive sum (a decoupled look-back; the wait is bounded
+//       and reports a stall);
+//     - position = digit base (a 256-entry scan of the digit totals) + keys
+//       of the digit in lower tiles + the rank in the tile;
+//     three kernels (more tiles):
+//     - hist: per tile, a 256-bin histogram -> hist[digit][tile];
+//     - dscan: one workgroup per digit, an exclusive scan of that digit's
+//       counts over the tiles and the digit's total;
+//     - scatter: the same ranking and position, with the lower tiles' count
+//       read from the scanned histogram;
 //   prefix   inclusive u64 scan of block bytes in eviction order (tile scans,
 //            one-workgroup scan of tile totals, fix-up) and the number of
 //            evictions that frees the requested bytes.
@@ -42,6 +57,15 @@ constexpr int ENW = ET / 64;            // waves per tile workgroup
 constexpr uint32_t SMALL_SORT = 1u << 19;
 inline int keys_per_thread(uint32_t N) { return N <= SMALL_SORT ? 4 : 8; }
 constexpr uint64_t TIME_LIMIT = 1ull << 62;
+constexpr uint32_t KEY_WG_MAX = 128;     // workgroups of the keys kernel at most (one digit-count set each)
+constexpr uint32_t TOT_SPLIT = 8;        // totals: workgroups per pass, each summing a share of the sets
+// Tile counts up to this use one look-back kernel per pass, more use three
+// kernels (histogram, per-digit scan, scatter): each look-back round is a
+// device-coherent load, so the look-back chains grow with the tile count.
+constexpr uint32_t ONESWEEP_TILES = 128;
+constexpr uint64_t ST_AGG = 1ull << 32;  // status flags: the tile's own count ...
+constexpr uint64_t ST_INCL = 2ull << 32; // ... or its inclusive count over tiles 0..t
+constexpr uint32_t SPIN_LIMIT = 1u << 22;  // polls of one status word before reporting a stall
 
 struct EvictArgs {
   uint32_t N, ntiles, tier;
@@ -51,8 +75,14 @@ struct EvictArgs {
   uint64_t unit_bytes, need;
   uint64_t* keys[2];
   uint32_t* vals[2];
-  uint32_t* hist;       // [256][ntiles]
-  uint32_t* dtot;       // [256] keys per digit
+  uint32_t* hist;       // [256][ntiles] (three-kernel passes)
+  uint32_t* dtot;       // [256] keys per digit (three-kernel passes)
+  uint32_t onesweep;    // passes are single look-back kernels (few tiles)
+  uint64_t* status[2];  // [ntiles][256] per pass: (flag << 32) | count; passes alternate the two
+  uint32_t* part;       // [key_wg][8][256] digit counts of each keys workgroup, all passes
+  uint32_t* gtot;       // [8][256] keys per digit, all passes
+  uint32_t key_wg;      // workgroups of the keys kernel
+  uint32_t* tile_ctr;   // [8] tiles taken in each pass
   uint64_t* tile_sum;   // [ntiles]
   uint64_t* misc;       // [0] OR of keys, [1] AND of keys, [2] error bits, [3] evictions short of need
   uint32_t* order;      // out [N]
@@ -60,31 +90,70 @@ struct EvictArgs {
   uint32_t* result;     // out [2]: count, error bits
 };
 
-__global__ void evict_init_kernel(EvictArgs a) {
-  a.misc[0] = 0;
-  a.misc[1] = ~0ull;
-  a.misc[2] = 0;
-  a.misc[3] = 0;
+__global__ __launch_bounds__(ET) void evict_init_kernel(EvictArgs a) {
+  // status of the first pass that runs, and the tile counters
+  for (uint64_t i = (uint64_t)blockIdx.x * ET + threadIdx.x; i < (uint64_t)a.ntiles * 256; i += (uint64_t)gridDim.x * ET)
+    a.status[0][i] = 0;
+  for (uint32_t i = blockIdx.x * ET + threadIdx.x; i < 8 * 256; i += gridDim.x * ET) a.gtot[i] = 0;
+  if (blockIdx.x == 0) {
+    if (threadIdx.x < 8) a.tile_ctr[threadIdx.x] = 0;
+    if (threadIdx.x == 0) {
+      a.misc[0] = 0;
+      a.misc[1] = ~0ull;
+      a.misc[2] = 0;
+      a.misc[3] = 0;
+    }
+  }
 }
 
 __global__ __launch_bounds__(ET) void evict_keys_kernel(EvictArgs a) {
   // position of each type label in the tier's eviction order (busy, idle, inactive)
   const uint32_t gpu_pos[3] = {2, 1, 0}, cpu_pos[3] = {1, 2, 0};
   const uint32_t* pos = a.tier == MORI_TIER_GPU ? gpu_pos : cpu_pos;
+  __shared__ uint32_t s_c[8][256];  // this workgroup's keys per (pass, digit)
+#pragma unroll
+  for (int k = 0; k < 8; ++k) s_c[k][threadIdx.x] = 0;
+  __syncthreads();
   uint64_t o = 0, n = ~0ull, err = 0;
-  for (uint32_t i = blockIdx.x * ET + threadIdx.x; i < a.N; i += gridDim.x * ET) {
-    const uint8_t t = a.type[i];
-    const uint64_t la = a.last_access[i];
-    if (t > MORI_TYPE_INACTIVE || la >= TIME_LIMIT) {
-      err |= MORI_DEV_BAD_BLOCK;
-      continue;
+  // uniform trip count: the cross-lane steps below need every lane of the wave
+  for (uint64_t i0 = (uint64_t)blockIdx.x * ET; i0 < a.N; i0 += (uint64_t)gridDim.x * ET) {
+    const uint64_t i = i0 + threadIdx.x;
+    bool valid = i < a.N;
+    uint64_t key = 0;
+    if (valid) {
+      const uint8_t t = a.type[i];
+      const uint64_t la = a.last_access[i];
+      if (t > MORI_TYPE_INACTIVE || la >= TIME_LIMIT) {
+        err |= MORI_DEV_BAD_BLOCK;
+        valid = false;
+      } else {
+        key = ((uint64_t)pos[t] << 62) | la;
+        a.keys[0][i] = key;
+        a.vals[0][i] = (uint32_t)i;
+        o |= key;
+        n &= key;
+      }
     }
-    const uint64_t key = ((uint64_t)pos[t] << 62) | la;
-    a.keys[0][i] = key;
-    a.vals[0][i] = i;
-    o |= key;
-    n &= key;
+    if (!a.onesweep) continue;  // uniform: the three-kernel passes count per tile
+    // runs of equal keys within the wave (the blocks of a program share their
+    // time): the first lane of a run adds the run's length for each digit
+    const int lane = threadIdx.x & 63;
+    const uint64_t prev = __shfl_up(key, 1, 64);
+    const bool prev_valid = __shfl_up(valid ? 1 : 0, 1, 64) != 0;
+    const bool head = valid && (lane == 0 || !prev_valid || prev != key);
+    const uint64_t heads = __ballot(head);
+    const uint64_t ends = heads | ~__ballot(valid);  // a run ends at the next head or invalid lane
+    if (head) {
+      const uint64_t later = lane == 63 ? 0ull : ends & ~((2ull << lane) - 1ull);
+      const uint32_t len = (later ? (uint32_t)__builtin_ctzll(later) : 64u) - (uint32_t)lane;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) atomicAdd(&s_c[k][(uint32_t)(key >> (8 * k)) & 255u], len);
+    }
   }
+  __syncthreads();
+  if (a.onesweep)
+#pragma unroll
+    for (int k = 0; k < 8; ++k) a.part[((uint64_t)blockIdx.x * 8 + k) * 256 + threadIdx.x] = s_c[k][threadIdx.x];
   // wave, then workgroup reduction: one set of global atomics per workgroup
   __shared__ uint64_t s_red[3][ENW];
   for (int off = 32; off > 0; off >>= 1) {
@@ -194,13 +263,6 @@ __global__ __launch_bounds__(ET) void evict_dscan_kernel(EvictArgs a, int shift)
   if (threadIdx.x == 0) a.dtot[blockIdx.x] = carry;
 }
 
-// Tile counts at or below this are scanned inside each scatter workgroup (its
-// thread d sums digit d over the tiles before its own and over all tiles), so
-// a pass is two launches instead of three.  Measured: at 4 tiles this saves a
-// fifth of the sort; at 69 tiles each thread's strided walk over its row costs
-// more than the launch it saves, so above 16 the separate scan runs.
-constexpr uint32_t INLINE_SCAN_TILES = 16;
-
 template <int EIPT>
 __global__ __launch_bounds__(ET) void evict_scatter_kernel(EvictArgs a, int shift) {
   // s_cnt[slice][wave][digit]: keys of that digit in that wave's 64 keys of the
@@ -216,20 +278,9 @@ __global__ __launch_bounds__(ET) void evict_scatter_kernel(EvictArgs a, int shif
   uint32_t* vd = a.vals[src ^ 1];
   const uint64_t base = (uint64_t)blockIdx.x * (ET * EIPT);
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  uint32_t tot, before, total_d;
-  if (a.ntiles <= INLINE_SCAN_TILES) {  // raw counts: sum them here
-    const uint32_t* h = a.hist + (uint64_t)tid * a.ntiles;
-    before = 0;
-    total_d = 0;
-    for (uint32_t t = 0; t < a.ntiles; ++t) {
-      const uint32_t c = h[t];
-      before += t < blockIdx.x ? c : 0u;
-      total_d += c;
-    }
-  } else {  // scanned by evict_dscan_kernel
-    before = a.hist[(uint64_t)tid * a.ntiles + blockIdx.x];
-    total_d = a.dtot[tid];
-  }
+  uint32_t tot;
+  const uint32_t before = a.hist[(uint64_t)tid * a.ntiles + blockIdx.x];  // scanned by evict_dscan_kernel
+  const uint32_t total_d = a.dtot[tid];
   const uint32_t digit_base = scan256(total_d, s_w, &tot);
   s_off[tid] = digit_base + before;
 #pragma unroll
@@ -271,6 +322,143 @@ __global__ __launch_bounds__(ET) void evict_scatter_kernel(EvictArgs a, int shif
         run += c;
       }
   }
+  __syncthreads();
+#pragma unroll
+  for (int it = 0; it < EIPT; ++it) {
+    const uint32_t d = dig[it];
+    if (d < 256u) {
+      const uint32_t pos = s_off[d] + s_cnt[it][wid][d] + rnk[it];
+      kd[pos] = key[it];
+      vd[pos] = val[it];
+    }
+  }
+}
+
+// Keys per digit of every pass: workgroup (pass, share) sums a share of the
+// keys workgroups' counts, one digit per thread.
+__global__ __launch_bounds__(ET) void evict_totals_kernel(EvictArgs a) {
+  const uint32_t k = blockIdx.x / TOT_SPLIT, j = blockIdx.x % TOT_SPLIT;
+  uint32_t sum = 0;
+  for (uint32_t g = j; g < a.key_wg; g += TOT_SPLIT) sum += a.part[((uint64_t)g * 8 + k) * 256 + threadIdx.x];
+  if (sum) atomicAdd(&a.gtot[k * 256 + threadIdx.x], sum);
+}
+
+__device__ inline void status_store(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline uint64_t status_load(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// One pass of the sort (the digit at `shift`), one workgroup per tile.
+template <int EIPT>
+__global__ __launch_bounds__(ET) void evict_pass_kernel(EvictArgs a, int shift) {
+  // s_cnt[slice][wave][digit]: keys of that digit in that wave's 64 keys of the
+  // slice, then (after the per-digit scan) their offset within the tile
+  __shared__ uint16_t s_cnt[EIPT][ENW][256];
+  __shared__ uint32_t s_off[256];  // this tile's global base per digit
+  __shared__ uint32_t s_w[ENW];
+  __shared__ uint32_t s_tile;
+  if (a.misc[2] || !digit_varies(a, shift)) return;
+  const int src = source_buffer(a, shift);  // the parity of this pass among those that run
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  if (tid == 0) s_tile = atomicAdd(&a.tile_ctr[shift >> 3], 1u);
+#pragma unroll
+  for (int it = 0; it < EIPT; ++it)
+#pragma unroll
+    for (int w = 0; w < ENW; ++w) s_cnt[it][w][tid] = 0;
+  const uint32_t total_d = a.gtot[(shift >> 3) * 256 + tid];  // keys of this digit in all tiles
+  __syncthreads();
+  const uint32_t tile = s_tile;
+  // the next pass that runs uses the other status array; the previous one that
+  // used it has finished
+  a.status[src ^ 1][(uint64_t)tile * 256 + tid] = 0;
+  const uint64_t* ks = a.keys[src];
+  const uint32_t* vs = a.vals[src];
+  uint64_t* kd = a.keys[src ^ 1];
+  uint32_t* vd = a.vals[src ^ 1];
+  const uint64_t base = (uint64_t)tile * (ET * EIPT);
+  // rank of every key among the keys of its digit in its wave's slice (ballots)
+  const uint64_t lanemask_lt = (1ull << lane) - 1ull;
+  uint64_t key[EIPT];
+  uint32_t val[EIPT], dig[EIPT], rnk[EIPT];
+#pragma unroll
+  for (int it = 0; it < EIPT; ++it) {
+    const uint64_t i = base + it * ET + tid;
+    const bool valid = i < a.N;
+    key[it] = valid ? ks[i] : 0ull;
+    val[it] = valid ? vs[i] : 0u;
+    const uint32_t d = (uint32_t)(key[it] >> shift) & 255u;
+    uint64_t same = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const uint64_t bal = __ballot((d >> b) & 1u);
+      same &= ((d >> b) & 1u) ? bal : ~bal;
+    }
+    const uint32_t r = __popcll(same & lanemask_lt);
+    if (valid && r == 0) s_cnt[it][wid][d] = (uint16_t)__popcll(same);
+    dig[it] = valid ? d : 256u;
+    rnk[it] = r;
+  }
+  __syncthreads();
+  // per digit (one per thread): offsets in (slice, wave) order, i.e. original
+  // key order, and the tile's count of the digit
+  uint32_t run = 0;
+#pragma unroll
+  for (int it = 0; it < EIPT; ++it)
+#pragma unroll
+    for (int w = 0; w < ENW; ++w) {
+      const uint32_t c = s_cnt[it][w][tid];
+      s_cnt[it][w][tid] = (uint16_t)run;
+      run += c;
+    }
+  // publish, then look back over the lower tiles
+  uint64_t* st = a.status[src];
+  uint64_t* mine = st + (uint64_t)tile * 256 + tid;
+  uint32_t before = 0;
+  if (tile == 0) {
+    status_store(mine, ST_INCL | run);
+  } else {
+    status_store(mine, ST_AGG | run);
+    // rounds of eight tiles below the next unaccounted one, loaded at once and
+    // taken in order: counts add up until a tile holding its inclusive sum; a
+    // tile that has not published yet ends the round and is polled again
+    constexpr int LB = 8;
+    uint32_t next = tile;  // tiles next..tile-1 are accounted for
+    uint32_t spins = 0;
+    bool done = false;
+    while (!done) {
+      uint64_t w[LB];
+#pragma unroll
+      for (int j = 0; j < LB; ++j)
+        w[j] = next > (uint32_t)j ? status_load(st + (uint64_t)(next - 1 - j) * 256 + tid) : ST_INCL;
+      int used = 0;
+#pragma unroll
+      for (int j = 0; j < LB; ++j) {
+        if (used < j) break;  // an earlier entry of this round was not ready
+        const uint64_t flag = w[j] >> 32;
+        if (flag == 0) break;
+        before += (uint32_t)w[j];
+        used = j + 1;
+        if (flag == (ST_INCL >> 32)) {
+          done = true;
+          break;
+        }
+      }
+      next -= (uint32_t)used;
+      if (!done && used < LB) {  // the tile below `next` has not published yet
+        if (++spins > SPIN_LIMIT) {
+          atomicOr((unsigned long long*)&a.misc[2], (unsigned long long)MORI_DEV_STALL);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+    status_store(mine, ST_INCL | (uint64_t)(before + run));
+  }
+  uint32_t tot;
+  const uint32_t digit_base = scan256(total_d, s_w, &tot);
+  s_off[tid] = digit_base + before;
   __syncthreads();
 #pragma unroll
   for (int it = 0; it < EIPT; ++it) {
@@ -418,9 +606,13 @@ __global__ void evict_result_kernel(EvictArgs a) {
 template <int EIPT>
 void launch_tiles(const EvictArgs& a, hipStream_t s) {
   for (int shift = 0; shift < 64; shift += 8) {
-    hipLaunchKernelGGL(evict_hist_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a, shift);
-    if (a.ntiles > INLINE_SCAN_TILES) hipLaunchKernelGGL(evict_dscan_kernel, dim3(256), dim3(ET), 0, s, a, shift);
-    hipLaunchKernelGGL(evict_scatter_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a, shift);
+    if (a.onesweep) {
+      hipLaunchKernelGGL(evict_pass_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a, shift);
+    } else {
+      hipLaunchKernelGGL(evict_hist_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a, shift);
+      hipLaunchKernelGGL(evict_dscan_kernel, dim3(256), dim3(ET), 0, s, a, shift);
+      hipLaunchKernelGGL(evict_scatter_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a, shift);
+    }
   }
   hipLaunchKernelGGL(evict_prefix_tiles_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a);
   hipLaunchKernelGGL(evict_prefix_top_kernel, dim3(1), dim3(1024), 0, s, a);
@@ -433,8 +625,8 @@ uint64_t evict_workspace_bytes(uint32_t N) {
   const uint64_t tile = (uint64_t)ET * keys_per_thread(N);
   const uint64_t ntiles = ((uint64_t)N + tile - 1) / tile;
   auto up = [](uint64_t b) { return (b + 255) & ~255ull; };
-  return 2 * up(8ull * N) + 2 * up(4ull * N) + up(4ull * 256 * ntiles) + up(4 * 256) + up(8ull * ntiles) +
-         up(8ull * N) + up(8 * 4);
+  return 2 * up(8ull * N) + 2 * up(4ull * N) + up(4ull * 256 * ntiles) + up(4 * 256) + 2 * up(8ull * 256 * ntiles) +
+         up(4ull * KEY_WG_MAX * 8 * 256) + up(4 * 8 * 256) + up(4 * 8) + up(8ull * ntiles) + up(8ull * N) + up(8 * 4);
 }
 
 hipError_t launch_evict(uint32_t N, const uint8_t* type, const uint64_t* last_access, const uint32_t* size,
@@ -465,6 +657,17 @@ hipError_t launch_evict(uint32_t N, const uint8_t* type, const uint64_t* last_ac
   w += up(4ull * 256 * a.ntiles);
   a.dtot = reinterpret_cast<uint32_t*>(w);
   w += up(4 * 256);
+  a.onesweep = a.ntiles <= ONESWEEP_TILES;
+  for (int b = 0; b < 2; ++b) {
+    a.status[b] = reinterpret_cast<uint64_t*>(w);
+    w += up(8ull * 256 * a.ntiles);
+  }
+  a.part = reinterpret_cast<uint32_t*>(w);
+  w += up(4ull * KEY_WG_MAX * 8 * 256);
+  a.gtot = reinterpret_cast<uint32_t*>(w);
+  w += up(4 * 8 * 256);
+  a.tile_ctr = reinterpret_cast<uint32_t*>(w);
+  w += up(4 * 8);
   a.tile_sum = reinterpret_cast<uint64_t*>(w);
   w += up(8ull * a.ntiles);
   uint64_t* prefix_tmp = reinterpret_cast<uint64_t*>(w);
@@ -474,8 +677,10 @@ hipError_t launch_evict(uint32_t N, const uint8_t* type, const uint64_t* last_ac
   a.prefix = prefix ? prefix : prefix_tmp;
   a.result = result;
   const uint32_t tiles = a.ntiles ? a.ntiles : 1;
-  hipLaunchKernelGGL(evict_init_kernel, dim3(1), dim3(1), 0, s, a);
-  hipLaunchKernelGGL(evict_keys_kernel, dim3(tiles < 1024 ? tiles : 1024), dim3(ET), 0, s, a);
+  hipLaunchKernelGGL(evict_init_kernel, dim3(tiles < 256 ? tiles : 256), dim3(ET), 0, s, a);
+  a.key_wg = tiles < KEY_WG_MAX ? tiles : KEY_WG_MAX;
+  hipLaunchKernelGGL(evict_keys_kernel, dim3(a.key_wg), dim3(ET), 0, s, a);
+  if (a.onesweep) hipLaunchKernelGGL(evict_totals_kernel, dim3(8 * TOT_SPLIT), dim3(ET), 0, s, a);
   if (a.ntiles) {
     if (kpt == 4) launch_tiles<4>(a, s);
     else launch_tiles<8>(a, s);

@@ -17,6 +17,7 @@ MORI_OK, MORI_EINVAL, MORI_ENOSPC, MORI_ESTATE, MORI_EHIP, MORI_EDEVICE = 0, -1,
 MORI_DEV_BAD_WINDOW, MORI_DEV_BAD_IDLENESS, MORI_DEV_BAD_TIER, MORI_DEV_BAD_TBL_OFF = 0x1, 0x2, 0x4, 0x8
 MORI_DEV_PAGE_RANGE, MORI_DEV_PAGE_DUP, MORI_DEV_PAGE_LEAK, MORI_DEV_NONRES_PAGE = 0x10, 0x20, 0x40, 0x80
 MORI_DEV_NOSPC, MORI_DEV_HOST_ADDR, MORI_DEV_BAD_BLOCK, MORI_DEV_BAD_STATUS = 0x100, 0x200, 0x400, 0x800
+MORI_DEV_STALL = 0x1000
 MORI_TYPE_BUSY, MORI_TYPE_IDLE, MORI_TYPE_INACTIVE = 0, 1, 2
 MORI_TIER_GPU, MORI_TIER_CPU, MORI_TIER_WAIT, MORI_TIER_SSD = 0, 1, 2, 3
 MORI_NO_PAGE = 0xFFFFFFFF

@@ -67,7 +67,7 @@ def test_degenerate_keys():
     check(np.full(N, 2, np.uint8), np.full(N, (1 << 62) - 1, np.uint64), None, 1, 0, N + 5)
 
 
-@pytest.mark.parametrize("N", [69938, 1 << 20])
+@pytest.mark.parametrize("N", [69938, 131072, 300000, 1 << 20])  # look-back passes up to 131072, three kernels above
 def test_large(N):
     rng = np.random.default_rng(N)
     typ, la, size = eviction_blocks(rng, N, programs=1024, tie_frac=0.5)
