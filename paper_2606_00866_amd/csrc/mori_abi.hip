@@ -485,6 +485,39 @@ int stage_addresses(mori_ctx* c, int d, const uint64_t* addr, hipStream_t s) {
   return MORI_OK;
 }
 
+// Copies of one staging half, issued in unit order; a segment that continues
+// the previous one on both sides (host buffers of consecutive programs that
+// are adjacent, as a first-fit arena hands them out) joins it, so a half
+// takes as few copy-engine commands as its host layout allows.
+struct CopyRun {
+  uint8_t* dst = nullptr;
+  const uint8_t* src = nullptr;
+  uint64_t bytes = 0;
+};
+
+int copy_flush(mori_ctx* c, CopyRun& r, hipMemcpyKind kind, hipStream_t s) {
+  if (r.bytes) HIP_TRY(c, hipMemcpyAsync(r.dst, r.src, r.bytes, kind, s));
+  r.bytes = 0;
+  return MORI_OK;
+}
+
+int copy_add(mori_ctx* c, CopyRun& r, uint8_t* dst, const uint8_t* src, uint64_t bytes, hipMemcpyKind kind,
+             hipStream_t s) {
+  if (r.bytes && r.dst + r.bytes == dst && r.src + r.bytes == src) {
+    // joined only inside one registered range: one allocation for the copy
+    const uint64_t host = reinterpret_cast<uint64_t>(kind == hipMemcpyDeviceToHost ? r.dst : r.src);
+    if (find_range(c, host, r.bytes + bytes)) {
+      r.bytes += bytes;
+      return MORI_OK;
+    }
+  }
+  if (int rc = copy_flush(c, r, kind, s)) return rc;
+  r.dst = dst;
+  r.src = src;
+  r.bytes = bytes;
+  return MORI_OK;
+}
+
 SwapArgs swap_args(const mori_ctx* c, int d) {
   SwapArgs a{};
   a.pool = static_cast<uint8_t*>(c->pool.base);
@@ -589,13 +622,16 @@ extern "C" int mori_kv_swap_out(mori_ctx* ctx, const uint64_t* host_dst, uint32_
       HIP_TRY(ctx, hipEventRecord(ctx->ev_half_ready[0][h], s));
       HIP_TRY(ctx, hipStreamWaitEvent(cs, ctx->ev_half_ready[0][h], 0));
       while (j < n && (uint64_t)base[j + 1] * LC <= u0) ++j;
+      CopyRun cr;
       for (uint32_t k = j; k < n && (uint64_t)base[k] * LC < u1; ++k) {
         const uint64_t b0 = (uint64_t)base[k] * LC, b1 = (uint64_t)base[k + 1] * LC;
         const uint64_t lo = std::max(u0, b0), hi = std::min(u1, b1);
         if (hi <= lo) continue;
         uint8_t* dst = reinterpret_cast<uint8_t*>(host_dst[progs[k]]) + (lo - b0) * run;
-        HIP_TRY(ctx, hipMemcpyAsync(dst, half + (lo - u0) * run, (hi - lo) * run, hipMemcpyDeviceToHost, cs));
+        if (int rc = copy_add(ctx, cr, dst, half + (lo - u0) * run, (hi - lo) * run, hipMemcpyDeviceToHost, cs))
+          return rc;
       }
+      if (int rc = copy_flush(ctx, cr, hipMemcpyDeviceToHost, cs)) return rc;
       HIP_TRY(ctx, hipEventRecord(ctx->ev_half_free[0][h], cs));
     }
     // join: the copy stream's last copy implies all earlier ones
@@ -663,13 +699,16 @@ extern "C" int mori_kv_swap_in(mori_ctx* ctx, const uint64_t* host_src, uint32_t
       uint8_t* half = ctx->staging[1] + (uint64_t)h * cu * run;
       if (c >= 2) HIP_TRY(ctx, hipStreamWaitEvent(cs, ctx->ev_half_free[1][h], 0));
       while (j < n && (uint64_t)base[j + 1] * LC <= u0) ++j;
+      CopyRun cr;
       for (uint32_t k = j; k < n && (uint64_t)base[k] * LC < u1; ++k) {
         const uint64_t b0 = (uint64_t)base[k] * LC, b1 = (uint64_t)base[k + 1] * LC;
         const uint64_t lo = std::max(u0, b0), hi = std::min(u1, b1);
         if (hi <= lo) continue;
         const uint8_t* src = reinterpret_cast<const uint8_t*>(host_src[progs[k]]) + (lo - b0) * run;
-        HIP_TRY(ctx, hipMemcpyAsync(half + (lo - u0) * run, src, (hi - lo) * run, hipMemcpyHostToDevice, cs));
+        if (int rc = copy_add(ctx, cr, half + (lo - u0) * run, src, (hi - lo) * run, hipMemcpyHostToDevice, cs))
+          return rc;
       }
+      if (int rc = copy_flush(ctx, cr, hipMemcpyHostToDevice, cs)) return rc;
       HIP_TRY(ctx, hipEventRecord(ctx->ev_half_ready[1][h], cs));
       HIP_TRY(ctx, hipStreamWaitEvent(s, ctx->ev_half_ready[1][h], 0));
       if (!waited && u1 > u_recycled) {
