@@ -111,7 +111,7 @@ def cpu_baseline(cfg, cpu_frac: float, seconds: float, evict_sizes=(), plan_case
                       f"bidirectional rebalances, memcpy per run between host buffers, single thread")}
     # the same oracle on all of this process's cores: one thread per core, each
     # rebalancing its own copy of a smaller sample (the C oracle runs outside
-    # the GIL and its boundary path shares no state between calls)
+    # the GIL and shares no state between calls)
     import threading
 
     threads = max(1, min(16, len(os.sched_getaffinity(0))))

@@ -45,7 +45,8 @@ __global__ __launch_bounds__(WG) void pages_claim_kernel(PlanArgs a) {
   if (a.sum->error) return;
   const uint32_t used = a.tbl_off[a.P];
   uint32_t err = 0;
-  for (uint32_t e = blockIdx.x * WG + threadIdx.x; e < used; e += gridDim.x * WG) {
+  for (uint64_t e64 = (uint64_t)blockIdx.x * WG + threadIdx.x; e64 < used; e64 += (uint64_t)gridDim.x * WG) {
+    const uint32_t e = (uint32_t)e64;  // 64-bit stride: no wrap near 2^32 entries
     const uint32_t p = find_program(a.tbl_off, a.P, e);
     const uint32_t pg = a.tbl[e];
     if (a.tier_old[p] != MORI_TIER_GPU) {
@@ -207,7 +208,8 @@ __global__ __launch_bounds__(WG) void pages_assign_kernel(PlanArgs a) {
 __global__ __launch_bounds__(WG) void commit_kernel(PlanArgs a) {
   if (a.sum->error) return;
   const uint32_t used = a.tbl_off[a.P];
-  for (uint32_t e = blockIdx.x * WG + threadIdx.x; e < used; e += gridDim.x * WG) {
+  for (uint64_t e64 = (uint64_t)blockIdx.x * WG + threadIdx.x; e64 < used; e64 += (uint64_t)gridDim.x * WG) {
+    const uint32_t e = (uint32_t)e64;  // 64-bit stride: no wrap near 2^32 entries
     const uint32_t p = find_program(a.tbl_off, a.P, e);
     const uint8_t c = a.cat[p];
     if (c == MORI_CAT_OUT || c == MORI_CAT_DROP_GPU) a.tbl[e] = MORI_NO_PAGE;
