@@ -21,3 +21,21 @@ def test_help_lists_the_driver_flags():
     assert r.returncode == 0
     for flag in ("--gpus", "--steps", "--warmup", "--workload", "--schedule"):
         assert flag in r.stdout
+
+
+def test_link_bound_is_a_lower_bound_per_step():
+    """The per-step link bound: each direction alone at its one-way rate, both
+    within the two-way capacity; the largest of the three is the bound."""
+    sys.path.insert(0, ROOT)
+    import bench
+
+    pk = {"d2h_GBps": 50.0, "h2d_GBps": 60.0, "bidir_GBps": 100.0}
+    assert bench.link_bound_s(0, 0, pk) == 0.0
+    assert bench.link_bound_s(10e9, 0, pk) == 10e9 / 50e9               # one-way D2H
+    assert bench.link_bound_s(0, 12e9, pk) == 12e9 / 60e9               # one-way H2D
+    assert bench.link_bound_s(20e9, 20e9, pk) == 40e9 / 100e9           # balanced: the two-way capacity
+    assert bench.link_bound_s(30e9, 1e9, pk) == 30e9 / 50e9             # D2H-heavy: its own rate
+    # never below any of the three single limits
+    for o, i in ((1e9, 2e9), (7e9, 3e9), (5e9, 5e9)):
+        t = bench.link_bound_s(o, i, pk)
+        assert t >= o / 50e9 and t >= i / 60e9 and t >= (o + i) / 100e9
