@@ -196,27 +196,40 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     key[it] = ~0ull;  // padding sorts after every real key
     id[it] = x;
     if (x >= P) continue;
+    // every load of the program first, none behind a branch, so they are in
+    // flight together: one memory latency instead of one per load
+    const bool given = (a.flags & MORI_F_IDLENESS_GIVEN) != 0;
+    const bool need_status = incremental || (a.flags & MORI_F_STATUS_KEY);
     const uint8_t told = a.tier[x];
     const uint32_t off0 = a.tbl_off[x], off1 = a.tbl_off[x + 1];
+    const uint8_t st = need_status ? a.status[x] : 0;
+    float rv[8], cv[8];  // the first eight cycles of the window (clamped indices: k >= 1)
+    const float* w = given ? nullptr : a.window + (size_t)x * a.k * 2;
+    if (!given) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t j = min((uint32_t)u, a.k - 1);
+        rv[u] = w[2 * j];
+        cv[u] = w[2 * j + 1];
+      }
+    }
     if (told > top_tier) err |= MORI_DEV_BAD_TIER;
     if (off1 < off0) err |= MORI_DEV_BAD_TBL_OFF;
     s_nblk[x] = off1 - off0;
     s_told[x] = told;
     float v;
-    if (a.flags & MORI_F_IDLENESS_GIVEN) {
+    if (given) {
       v = a.idleness[x];
       if (!(v >= 0.0f && v <= 1.0f)) err |= MORI_DEV_BAD_IDLENESS;
     } else {
       float t_reasoning = 0.0f, t_acting = 0.0f;
-      const float* w = a.window + (size_t)x * a.k * 2;
       for (uint32_t j0 = 0; j0 < a.k; j0 += 8) {  // eight cycles' loads in flight, then the sums in order
-        float rv[8], cv[8];
+        if (j0 > 0) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          rv[u] = cv[u] = 0.0f;
-          if (j0 + u < a.k) {
-            rv[u] = w[2 * (j0 + u)];
-            cv[u] = w[2 * (j0 + u) + 1];
+          for (int u = 0; u < 8; ++u) {
+            const uint32_t j = min(j0 + u, a.k - 1);
+            rv[u] = w[2 * j];
+            cv[u] = w[2 * j + 1];
           }
         }
 #pragma unroll
@@ -237,7 +250,6 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     const uint32_t bits = __float_as_uint(v);  // < 2^30 for idleness in [0, 1]
     uint64_t k;
     if (incremental) {
-      const uint8_t st = a.status[x];
       if (st > MORI_ST_NEW) err |= MORI_DEV_BAD_STATUS;
       const uint64_t acting = st == MORI_ST_ACTING;
       uint64_t grp;
@@ -256,7 +268,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
       k = (grp << GROUP_SHIFT) | sub;
     } else {
       k = bits;
-      if ((a.flags & MORI_F_STATUS_KEY) && a.status[x] == MORI_ST_ACTING) k |= 0x80000000u;
+      if ((a.flags & MORI_F_STATUS_KEY) && st == MORI_ST_ACTING) k |= 0x80000000u;
     }
     key[it] = k;
     k_or |= k;
