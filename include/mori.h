@@ -30,7 +30,10 @@
  *     mori_plan_wait and mori_query.
  *   - Streams are hipStream_t values passed as void*; NULL is the default
  *     stream.  The library never synchronises the device.  It blocks the host
- *     only in mori_plan_wait and in copy-engine swaps (which need the plan).
+ *     in mori_plan_wait, in copy-engine swaps (which need the plan), in
+ *     mori_query(MORI_Q_DEVICE_ERROR), mori_profile_read, mori_register and
+ *     mori_destroy; a kernel-mode swap waits until the previous one of its
+ *     direction has read its address table.
  *   - Ownership: the caller owns the pool, the program arrays, the host
  *     buffers and the streams.  The context owns its device scratch, a small
  *     pinned mirror of the plan and, for copy-engine swaps, device staging
@@ -326,7 +329,7 @@ typedef struct {
 } mori_blocks;
 
 /* Bytes of device workspace mori_evict_order needs for num_blocks blocks
- * (about 32 bytes per block). */
+ * (about 36 bytes per block, plus 1 MiB). */
 int mori_evict_workspace(uint32_t num_blocks, uint64_t* bytes);
 
 /* Eviction order of one tier (MORI_TIER_GPU or MORI_TIER_CPU), enqueued on
