@@ -436,3 +436,60 @@ def test_two_contexts_interleaved():
     finally:
         for pair in pairs:
             pair.close()
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_no_writes_outside_the_pool_and_buffers(mode):
+    """Guard bytes around the pool (inside one larger allocation) and past the
+    end of the host arena's used extents keep their pattern through several
+    rebalances in both directions: no kernel writes outside the pages and
+    buffers the plan names."""
+    from workload import fill_pool_np, make_bank, program_host_content
+
+    rng = np.random.default_rng(91)
+    geom = Geometry(layers=2, planes=2, block_tokens=2, row_bytes=64, num_blocks=0)
+    inst = random_instance(rng, P=40, max_blocks=12, geom=geom, tier_p=(0.55, 0.45), extra_free=10)
+    g, bb = inst.geom, inst.geom.block_bytes
+    guard = 1 << 16
+    big = torch.full((guard + g.pool_bytes + guard,), 0xA5, dtype=torch.uint8, device="cuda")
+    pool_view = big[guard:guard + g.pool_bytes]
+    bank = make_bank(4, inst.dtype, g.run_bytes)
+    pool = fill_pool_np(inst, bank)
+    pool_view.copy_(torch.from_numpy(pool).cuda())
+    bufs = [program_host_content(inst, bank, p).copy() if inst.tier[p] == 1
+            else np.zeros(int(inst.nblk[p]) * bb, np.uint8) for p in range(inst.P)]
+    tbl, tier, free = inst.copy_state()
+    need = sum(max(4096, -(-int(n) * bb // 4096) * 4096) for n in inst.nblk)  # the arena's first-fit extents
+    tail = 1 << 16
+    tp = TierPool(g, inst.tbl_off, inst.tbl, inst.tier, inst.free_map, arena_bytes=need + tail, pool=pool_view)
+    try:
+        for p in range(inst.P):  # every program keeps one extent for the whole test
+            tp.give_host_buffer(p)
+            if bufs[p].size:
+                tp.host_view(p)[:] = bufs[p]
+        tail_view = tp.arena.view(tp.arena.ptr + need, tail)
+        tail_view[:] = 0x5A
+        s_out, s_in = torch.cuda.Stream(), torch.cuda.Stream()
+        for step in range(4):
+            w = inst.window if step % 2 == 0 else inst.window[:, :, ::-1].copy()
+            bg = int(rng.integers(g.num_blocks // 4, g.num_blocks + 1)) * bb
+            res = oracle.rebalance(g, window=w, tbl_off=inst.tbl_off, tbl=tbl, tier=tier, free_map=free,
+                                   gpu_budget=bg, cpu_budget=inst.total_bytes, pool=pool, host_bufs=bufs)
+            assert res.rc == oracle.OK
+            assert tp.rank_partition(gpu_bytes=bg, cpu_bytes=inst.total_bytes,
+                                     window=torch.from_numpy(np.ascontiguousarray(w)).cuda(), stream=s_out) == 0
+            rc, plan = tp.plan_wait()
+            assert rc == M.MORI_OK
+            assert tp.swap_out(mode, s_out) == M.MORI_OK
+            assert tp.swap_in(mode, s_in) == M.MORI_OK
+            torch.cuda.synchronize()
+            log(f"  guards step {step}: out {plan.n_out} in {plan.n_in}")
+            assert (big[:guard] == 0xA5).all().item() and (big[guard + g.pool_bytes:] == 0xA5).all().item()
+            assert (tail_view == 0x5A).all()
+            t_, r_, f_ = tp.state()
+            assert (t_ == tbl).all() and (r_ == tier).all() and (f_ == free).all()
+            for p in np.flatnonzero(tier == 1):
+                assert np.array_equal(tp.host_view(int(p)), bufs[p]), p
+    finally:
+        torch.cuda.synchronize()
+        tp.close()
