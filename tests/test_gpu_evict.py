@@ -110,3 +110,29 @@ def test_bench_inputs(N):
     typ, la, size, need = bench.evict_inputs(np, N)
     log(f"evict bench inputs N={N}")
     check(typ, la, size, 4096, 0, need)
+
+
+@pytest.mark.parametrize("N", [1000, 69938, 300000])
+def test_no_writes_past_outputs_or_workspace(N):
+    """Sentinels past order[N], prefix[N], result[2] and the workspace's stated
+    size are untouched (both radix pass forms)."""
+    rng = np.random.default_rng(N + 5)
+    typ, la, size = eviction_blocks(rng, N, programs=300, tie_frac=0.4, var_size=True)
+    dev = "cuda"
+    t = torch.from_numpy(typ).to(dev)
+    l = torch.from_numpy(la.view(np.int64)).to(dev)
+    sz = torch.from_numpy(size.view(np.int32)).to(dev)
+    rc, wbytes = M.mori_evict_workspace(N)
+    assert rc == 0
+    pad = 4096
+    ws = torch.full((wbytes + pad,), 0x3C, dtype=torch.uint8, device=dev)
+    order = torch.full((N + 64,), -7, dtype=torch.int32, device=dev)
+    prefix = torch.full((N + 64,), -9, dtype=torch.int64, device=dev)
+    result = torch.full((2 + 14,), -11, dtype=torch.int32, device=dev)
+    blk = M.mori_blocks(N, t.data_ptr(), l.data_ptr(), sz.data_ptr(), 1)
+    assert M.mori_evict_order(blk, 0, N // 3, ws.data_ptr(), wbytes, order.data_ptr(), prefix.data_ptr(),
+                              result.data_ptr(), torch.cuda.current_stream().cuda_stream) == M.MORI_OK
+    torch.cuda.synchronize()
+    assert (order[N:] == -7).all().item() and (prefix[N:] == -9).all().item() and (result[2:] == -11).all().item()
+    assert (ws[wbytes:] == 0x3C).all().item()
+    assert result[1].item() == 0
