@@ -1,6 +1,6 @@
 """libmori's multi-replica admission (host code behind the C ABI) against the
 oracle, element by element, on random Waiting queues: up to 4096 programs
-with ties in size and idleness, 1 to 64 replicas, both replica rules; and its
+with ties in size and idleness, 1 to 1024 replicas, both replica rules; and its
 argument checks.  No GPU is involved."""
 import numpy as np
 import pytest
@@ -12,7 +12,7 @@ from paper_2606_00866_amd import mori as M
 def test_matches_oracle(orc, seed):
     rng = np.random.default_rng(7000 + seed)
     P = int(rng.choice([0, 1, 7, 100, 1000, 4096]))
-    R = int(rng.choice([1, 2, 3, 8, 64]))
+    R = int(rng.choice([1, 2, 3, 8, 64, 1024]))  # 1024: the maximum
     sizes = rng.integers(0, 40, P) * int(rng.choice([1, 2 << 20]))  # ties in size
     iota = rng.choice(np.array([0, 0.25, 0.5, 1], np.float32), P) if seed % 2 else rng.random(P).astype(np.float32)
     st = rng.choice(3, P, p=[0.5, 0.2, 0.3]).astype(np.uint8)
