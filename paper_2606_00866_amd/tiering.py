@@ -254,6 +254,33 @@ class TierPool:
         self.arena.close()
 
 
+def evict_order(block_type: torch.Tensor, last_access: torch.Tensor, size: torch.Tensor | None = None,
+                unit_bytes: int = 1, tier: int = M.MORI_TIER_GPU, need_bytes: int = 0, stream=None,
+                workspace: torch.Tensor | None = None):
+    """Typed eviction order of one tier (Sec. 4.3.2) for device tensors of block
+    metadata: type uint8 [N] (MORI_TYPE_*), last access int64 [N] (< 2^62), size
+    int32 [N] in units of unit_bytes or None.  Returns device tensors (order
+    int32 [N]: block evicted j-th; prefix int64 [N]: bytes freed by the first
+    j+1; result int32 [2]: fewest evictions freeing need_bytes, error bits),
+    enqueued on `stream`.  The workspace is allocated here unless given."""
+    N = int(block_type.numel())
+    dev = block_type.device
+    assert last_access.numel() == N and (size is None or size.numel() == N)
+    rc, wbytes = M.mori_evict_workspace(N)
+    check(rc, "mori_evict_workspace")
+    if workspace is None:
+        workspace = torch.empty(max(wbytes, 256), dtype=torch.uint8, device=dev)
+    order = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
+    prefix = torch.empty(max(N, 1), dtype=torch.int64, device=dev)
+    result = torch.zeros(2, dtype=torch.int32, device=dev)
+    blk = M.mori_blocks(N, block_type.data_ptr() if N else None, last_access.data_ptr() if N else None,
+                        size.data_ptr() if size is not None else None, int(unit_bytes))
+    check(M.mori_evict_order(blk, int(tier), int(need_bytes), workspace.data_ptr(), workspace.numel(),
+                             order.data_ptr(), prefix.data_ptr(), result.data_ptr(), _stream(stream)),
+          "mori_evict_order")
+    return order[:N], prefix[:N], result
+
+
 def _stream(s) -> int:
     if s is None:
         return torch.cuda.current_stream().cuda_stream

@@ -136,3 +136,22 @@ def test_no_writes_past_outputs_or_workspace(N):
     assert (order[N:] == -7).all().item() and (prefix[N:] == -9).all().item() and (result[2:] == -11).all().item()
     assert (ws[wbytes:] == 0x3C).all().item()
     assert result[1].item() == 0
+
+
+def test_python_wrapper():
+    """tiering.evict_order (device tensors in, device tensors out) equals the oracle."""
+    from paper_2606_00866_amd.tiering import evict_order
+
+    rng = np.random.default_rng(321)
+    N = 5000
+    typ, la, size = eviction_blocks(rng, N, programs=50, tie_frac=0.5, var_size=True)
+    need = int(size.astype(np.int64).sum()) * 4096 // 3
+    order, prefix, result = evict_order(torch.from_numpy(typ).cuda(), torch.from_numpy(la.view(np.int64)).cuda(),
+                                        torch.from_numpy(size.view(np.int32)).cuda(), unit_bytes=4096,
+                                        tier=M.MORI_TIER_CPU, need_bytes=need)
+    torch.cuda.synchronize()
+    rc, o_order, o_prefix, o_count = oracle.evict_order(typ, la, M.MORI_TIER_CPU, need, size=size, unit_bytes=4096)
+    assert rc == oracle.OK
+    assert np.array_equal(order.cpu().numpy().view(np.uint32), o_order)
+    assert np.array_equal(prefix.cpu().numpy().view(np.uint64), o_prefix)
+    assert result.cpu().tolist() == [o_count, 0]
