@@ -595,6 +595,13 @@ def main() -> int:
                      "kernel": dom["kernel"], "frac_of_measured_copy_peak":
                          round(achieved / peaks["d2d_copy_GBps"], 4)},
         "kernels": kern,
+        "paper_context": {
+            "end_to_end_throughput_vs_best_offloading_baseline": "+20% to +71%",
+            "average_ttft_vs_best_offloading_baseline": "-18% to -43%",
+            "hardware": "H200 (capped to 80 GB, and full) and B200 (TP=2), SGLang with HiCache",
+            "note": ("whole-system serving gains of the method, context only; the paper reports no KV migration "
+                     "or gather/scatter bandwidth, hence vs_baseline null"),
+        },
         "direction_ms_per_step": {"swap_out": round(span[0] / args.steps, 2), "swap_in": round(span[1] / args.steps, 2)},
         "plan_us_in_step": round(span[2] / args.steps * 1e3, 1),
         "plan": plan,
