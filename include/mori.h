@@ -34,6 +34,9 @@
  *     mori_query(MORI_Q_DEVICE_ERROR), mori_profile_read, mori_register and
  *     mori_destroy; a kernel-mode swap waits until the previous one of its
  *     direction has read its address table.
+ *   - Threads: a context is driven by one host thread at a time (its calls
+ *     are not synchronised against each other); distinct contexts share no
+ *     state, and mori_evict_order and mori_replica_admit keep none.
  *   - Ownership: the caller owns the pool, the program arrays, the host
  *     buffers and the streams.  The context owns its device scratch, a small
  *     pinned mirror of the plan and, for copy-engine swaps, device staging
