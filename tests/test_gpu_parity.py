@@ -493,3 +493,40 @@ def test_no_writes_outside_the_pool_and_buffers(mode):
     finally:
         torch.cuda.synchronize()
         tp.close()
+
+
+def test_two_contexts_on_two_host_threads():
+    """Two host threads, each driving its own context (own pool, streams and
+    arena) through three rebalances at the same time; each matches its own
+    oracle run (distinct contexts share no state)."""
+    import threading
+
+    insts = [random_instance(np.random.default_rng(500 + i), P=30, max_blocks=10,
+                             geom=Geometry(layers=2, planes=2, block_tokens=2, row_bytes=64, num_blocks=0),
+                             tier_p=(0.5, 0.35, 0.15), extra_free=8) for i in range(2)]
+    pairs = [Pair(inst, seed=60 + i) for i, inst in enumerate(insts)]
+    errors = []
+
+    def work(i):
+        try:
+            inst, pair = insts[i], pairs[i]
+            rng = np.random.default_rng(900 + i)
+            bb = inst.geom.block_bytes
+            for step in range(3):
+                bg = int(rng.integers(inst.geom.num_blocks // 3, inst.geom.num_blocks + 1)) * bb
+                w = inst.window if step % 2 == 0 else inst.window[:, :, ::-1].copy()
+                pair.step(gpu_bytes=bg, cpu_bytes=inst.total_bytes, window=w, mode=MODES[(i + step) % 2])
+        except BaseException as e:  # reported below
+            errors.append(repr(e))
+
+    try:
+        threads = [threading.Thread(target=work, args=(i,)) for i in range(2)]
+        for th in threads:
+            th.start()
+        for th in threads:
+            th.join(timeout=120)
+        assert not any(th.is_alive() for th in threads)
+        assert not errors, errors
+    finally:
+        for pair in pairs:
+            pair.close()
