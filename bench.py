@@ -178,13 +178,23 @@ def cpu_baseline(cfg, cpu_frac: float, seconds: float, evict_sizes=(), plan_case
         rc, *_ = oracle.evict_order(typ, la, 0, need, size=size, unit_bytes=4096)
         out["evict_order_us"][str(N)] = round((time.perf_counter() - t0) * 1e6, 1)
         assert rc == oracle.OK
+    out["replica_admit_us"] = []
+    for P, R in REPLICA_CASES:
+        sizes, iota, status, room = replica_inputs(np, P, R)
+        for rule, flags in (("most room", 0), ("best fit", oracle.ADMIT_BEST_FIT)):
+            t0 = time.perf_counter()
+            rc, *_ = oracle.replica_admit(sizes, iota, status, room, flags)
+            out["replica_admit_us"].append({"programs": P, "replicas": R, "rule": rule,
+                                            "us": round((time.perf_counter() - t0) * 1e6, 1)})
+            assert rc == oracle.OK
     out["plan_us"] = []
     for label, geom, src, gb, cb, status, wins in plan_cases:
-        for policy, flags in POLICIES:
+        for policy, flags, sfrac in POLICIES:
             tbl, tier, free = src.copy_state()
             t0 = time.perf_counter()
             res = oracle.rebalance(geom, window=wins[0], status=status, tbl_off=src.tbl_off, tbl=tbl, tier=tier,
-                                   free_map=free, gpu_budget=gb, cpu_budget=cb, flags=flags)
+                                   free_map=free, gpu_budget=gb, cpu_budget=cb, flags=flags,
+                                   ssd_budget=ssd_budget(src, sfrac))
             out["plan_us"].append({"case": label, "policy": policy,
                                    "us": round((time.perf_counter() - t0) * 1e6, 1)})
             assert res.rc == oracle.OK
@@ -347,12 +357,21 @@ def plan_cases(np, inst, bg, bc):
     return cases
 
 
-POLICIES = (("boundary", 0), ("incremental", 8))  # MORI_F_INCREMENTAL
+# (name, flags, SSD budget as a fraction of the case's KV bytes): the boundary
+# policy, the incremental policy (MORI_F_INCREMENTAL) and three tiers
+# (MORI_F_SSD_TIER, the SSD tier a quarter of the KV bytes)
+POLICIES = (("boundary", 0, 0.0), ("incremental", 8, 0.0), ("three-tier", 16, 0.25))
+
+
+def ssd_budget(src, frac: float) -> int:
+    """SSD budget of a plan case, in its 16-byte pages."""
+    return int(src.total_bytes // max(src.geom.block_bytes, 1) * frac) * 16
 
 
 def plan_leg(torch, np, M, cases, reps=30):
-    """The rank/partition step alone (Eq. 1, ranking, the boundary or the
-    incremental policy, page allocation, table rewrite), which is latency-bound:
+    """The rank/partition step alone (Eq. 1, ranking, the boundary policy, the
+    incremental policy or three tiers, page allocation, table rewrite), which is
+    latency-bound:
     device time of mori_rank_partition (events on its stream, median of `reps`
     calls alternating the two windows, each followed by its plan on the host).
     Exact parity with the oracle on these inputs is a GPU test; the oracle's
@@ -363,16 +382,17 @@ def plan_leg(torch, np, M, cases, reps=30):
     for label, geom, src, gb, cb, status, wins in cases:
         st_d = torch.from_numpy(status).cuda()
         wins_d = [torch.from_numpy(w).cuda() for w in wins]
-        for policy, flags in POLICIES:
+        for policy, flags, sfrac in POLICIES:
             tp = TierPool(geom, src.tbl_off, src.tbl, src.tier, src.free_map, arena_bytes=64 << 20,
                           max_programs=src.P, staging_bytes=1 << 20)
+            sb = ssd_budget(src, sfrac)
             s = torch.cuda.current_stream()
             times = []
             for i in range(reps + 2):
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 e0.record(s)
                 assert tp.rank_partition(gpu_bytes=gb, cpu_bytes=cb, window=wins_d[i % 2], status=st_d,
-                                         flags=flags, stream=s) == 0
+                                         flags=flags, stream=s, ssd_bytes=sb) == 0
                 e1.record(s)
                 rc, p = tp.plan_wait()
                 assert rc == 0, (label, policy, rc, p.device_error)
@@ -381,6 +401,42 @@ def plan_leg(torch, np, M, cases, reps=30):
             tp.close()
             out.append({"case": label, "programs": src.P, "pages": geom.num_blocks, "policy": policy,
                         "us": round(sorted(times[2:])[reps // 2], 1)})
+    return out
+
+
+REPLICA_CASES = ((4096, 8), (4096, 64))  # (Waiting programs, replicas)
+
+
+def replica_inputs(np, P: int, R: int):
+    """A shared Waiting queue for multi-replica admission: P programs with
+    lognormal KV sizes (whole 2 MiB blocks), random idleness, a quarter Acting
+    (they stay), a third of the rest new arrivals; R replicas whose free GPU
+    room totals about half the queue's bytes."""
+    rng = np.random.default_rng(P * 1000 + R)
+    blocks = np.clip(np.exp(np.log(2048) + 0.5 * rng.standard_normal(P)), 256, 16384).astype(np.int64)
+    sizes = (blocks * (2 << 20)).astype(np.uint64)
+    iota = rng.random(P).astype(np.float32)
+    status = np.where(rng.random(P) < 0.25, 1, np.where(rng.random(P) < 1 / 3, 2, 0)).astype(np.uint8)
+    room = (rng.random(R) * 2 * sizes.sum() * 0.5 / R).astype(np.uint64)
+    return sizes, iota, status, room
+
+
+def replica_leg(np, M, reps=20):
+    """Multi-replica admission of the shared Waiting queue (host code behind the
+    ABI): median wall time of `reps` calls, both replica rules.  Parity with the
+    oracle on these inputs is a CPU test; the oracle's time is in the CPU baseline."""
+    out = []
+    for P, R in REPLICA_CASES:
+        sizes, iota, status, room = replica_inputs(np, P, R)
+        for rule, flags in (("most room", 0), ("best fit", M.MORI_ADMIT_BEST_FIT)):
+            times = []
+            for _ in range(reps):
+                t0 = time.perf_counter()
+                rc, rep_, after = M.mori_replica_admit(sizes, iota, status, room, flags)
+                times.append((time.perf_counter() - t0) * 1e6)
+                assert rc == 0
+            out.append({"programs": P, "replicas": R, "rule": rule, "admitted": int((rep_ >= 0).sum()),
+                        "us": round(sorted(times)[reps // 2], 1)})
     return out
 
 
@@ -554,6 +610,9 @@ def main() -> int:
     plan = None if args.no_plan else plan_leg(torch, np, M, cases)
     if plan:
         log(f"plan: {plan}")
+    replica = None if args.no_plan else replica_leg(np, M)
+    if replica:
+        log(f"replica admission: {replica}")
 
     out = {
         "metric": "KV migration GB/s (D2H+H2D) vs host-link peak; gather/scatter HBM GB/s",
@@ -605,6 +664,7 @@ def main() -> int:
         "direction_ms_per_step": {"swap_out": round(span[0] / args.steps, 2), "swap_in": round(span[1] / args.steps, 2)},
         "plan_us_in_step": round(span[2] / args.steps * 1e3, 1),
         "plan": plan,
+        "replica_admit": replica,
         "cpu_baseline": cpu,
         "verify": verify,
         "evict_order": evict,

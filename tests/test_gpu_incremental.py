@@ -166,8 +166,9 @@ def test_device_validation_and_host_checks():
 
 def test_bench_plan_cases():
     """The rank/partition leg of bench.py times these exact inputs (the
-    Llama-3-8B programs and pool pages, and 4096 random programs) under both
-    policies: two consecutive plans, each compared with the oracle's."""
+    Llama-3-8B programs and pool pages, and 4096 random programs) under every
+    policy it times (boundary, incremental, three tiers): two consecutive
+    plans, each compared with the oracle's."""
     import bench
     from paper_2606_00866_amd.tiering import TierPool
     from workload import LLAMA3_8B, budget_bytes, make_instance
@@ -175,7 +176,8 @@ def test_bench_plan_cases():
     inst = make_instance(LLAMA3_8B)
     bg = budget_bytes(inst.total_bytes, LLAMA3_8B.gpu_pct)
     for label, geom, src, gb, cb, status, wins in bench.plan_cases(np, inst, bg, 28 << 30):
-        for policy, flags in bench.POLICIES:
+        for policy, flags, sfrac in bench.POLICIES:
+            sb = bench.ssd_budget(src, sfrac)
             log(f"bench plan case {label} {policy}")
             tp = TierPool(geom, src.tbl_off, src.tbl, src.tier, src.free_map, arena_bytes=64 << 20,
                           max_programs=src.P, staging_bytes=1 << 20)
@@ -184,10 +186,11 @@ def test_bench_plan_cases():
                 st_d = torch.from_numpy(status).cuda()
                 for i in range(2):
                     res = oracle.rebalance(geom, window=wins[i], status=status, tbl_off=src.tbl_off, tbl=tbl,
-                                           tier=tier, free_map=free, gpu_budget=gb, cpu_budget=cb, flags=flags)
+                                           tier=tier, free_map=free, gpu_budget=gb, cpu_budget=cb, flags=flags,
+                                           ssd_budget=sb)
                     assert res.rc == oracle.OK
                     assert tp.rank_partition(gpu_bytes=gb, cpu_bytes=cb, window=torch.from_numpy(wins[i]).cuda(),
-                                             status=st_d, flags=flags) == M.MORI_OK
+                                             status=st_d, flags=flags, ssd_bytes=sb) == M.MORI_OK
                     rc, p = tp.plan_wait()
                     assert rc == M.MORI_OK
                     arr = tp.plan_arrays(p)

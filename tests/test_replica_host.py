@@ -42,3 +42,18 @@ def test_argument_checks():
     # no programs: room unchanged
     rc, rep, after = M.mori_replica_admit([], [], [], [5, 6])
     assert rc == M.MORI_OK and rep.size == 0 and after.tolist() == [5, 6]
+
+
+def test_bench_inputs(orc):
+    """The multi-replica leg of bench.py times these exact inputs."""
+    import bench
+
+    for P, R in bench.REPLICA_CASES:
+        sizes, iota, status, room = bench.replica_inputs(np, P, R)
+        for flags in (0, M.MORI_ADMIT_BEST_FIT):
+            rc, rep, after = M.mori_replica_admit(sizes, iota, status, room, flags)
+            orc_rc, orc_rep, orc_after = orc.replica_admit(sizes, iota, status, room,
+                                                           orc.ADMIT_BEST_FIT if flags else 0)
+            assert rc == M.MORI_OK and orc_rc == orc.OK
+            assert np.array_equal(rep, orc_rep) and np.array_equal(after, orc_after)
+            assert 0 < (rep >= 0).sum() < P  # some admitted, some left waiting
