@@ -114,9 +114,10 @@ __device__ inline void cursor_set(const SwapArgs& s, Cursor& c, uint32_t a) {
 // Source and destination of unit u (u >= the cursor's unit); false when the
 // unit belongs to the other part of a two-part swap-in.
 template <bool kOut>
-__device__ inline bool unit_ends(const SwapArgs& s, uint32_t n, Cursor& c, uint64_t u, uint64_t u_lo, uint64_t nf,
-                                 const v4u** src, v4u** dst) {
-  while (u >= c.u_first + c.nb * s.LC) cursor_set(s, c, c.a + 1);  // never past n - 1 for u < total
+__device__ inline bool unit_ends(const SwapArgs& s, Cursor& c, uint64_t u, uint64_t u_lo, uint64_t nf, const v4u** src,
+                                 v4u** dst) {
+  // u < the direction's total units, so the cursor stops at its last program
+  while (u >= c.u_first + c.nb * s.LC) cursor_set(s, c, c.a + 1);
   const uint64_t rem = u - c.u_first;
   uint64_t q, i;
   if ((rem >> 32) == 0 && (c.nb >> 32) == 0) {  // the usual case: a 32-bit division
@@ -149,14 +150,14 @@ __global__ __launch_bounds__(NT) void swap_kernel(SwapArgs s) {
   cursor_set(s, c, find_slice(s.pg_base, n, u / s.LC));
   const v4u* src;
   v4u* dst;
-  bool ok = unit_ends<kOut>(s, n, c, u, lo, nf, &src, &dst);
+  bool ok = unit_ends<kOut>(s, c, u, lo, nf, &src, &dst);
   for (;;) {
     // decode the next unit first: its loads overlap this unit's copy
     const uint64_t un = u + gridDim.x;
     const v4u* nsrc = nullptr;
     v4u* ndst = nullptr;
     const bool more = un < hi;
-    const bool nok = more && unit_ends<kOut>(s, n, c, un, lo, nf, &nsrc, &ndst);
+    const bool nok = more && unit_ends<kOut>(s, c, un, lo, nf, &nsrc, &ndst);
     if (ok) copy_run(src, dst, n16, threadIdx.x);
     if (!more) break;
     u = un;
