@@ -33,7 +33,6 @@ os.environ["GPU_MAX_HW_QUEUES"] = _HWQ
 import argparse
 import ctypes as C
 import json
-import math
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))

@@ -8,7 +8,7 @@ import torch
 from gpu_helpers import Pair, log
 from oracle import oracle
 from paper_2606_00866_amd import mori as M
-from paper_2606_00866_amd.tiering import MoriError, TierPool
+from paper_2606_00866_amd.tiering import TierPool
 from workload import TINY, Geometry, budget_bytes, make_instance, random_instance
 
 pytestmark = pytest.mark.gpu
