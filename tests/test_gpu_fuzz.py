@@ -93,3 +93,42 @@ def test_eviction_sizes_around_the_pass_switch(N):
     need = int(rng.integers(0, total + 1)) * 7
     log(f"fuzz evict N={N} need={need}")
     check(typ, la, size, 7, int(N % 2), need)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_policy_changes_between_steps(seed):
+    """One pool whose policy changes from step to step (boundary, incremental,
+    skip-fit variants, given idleness, three tiers and back once no program is
+    left on the SSD tier): each step equals the oracle's from the same state."""
+    rng = np.random.default_rng(81000 + seed)
+    geom = Geometry(2, 2, 2, 48, 0)
+    inst = random_instance(rng, P=int(rng.choice([20, 200])), max_blocks=10, geom=geom, tier_p=(0.5, 0.3, 0.2),
+                           extra_free=int(rng.integers(2, 30)))
+    pair = Pair(inst, seed=seed, staging_bytes=int(rng.choice([0, 4 * inst.geom.run_bytes])))
+    try:
+        bb = inst.geom.block_bytes
+        nb_total = inst.total_bytes // bb
+        status = rng.integers(0, 3, inst.P).astype(np.uint8)
+        forms = [0, M.MORI_F_INCREMENTAL, M.MORI_F_SKIP_FIT, M.MORI_F_INCREMENTAL | M.MORI_F_SKIP_FIT,
+                 M.MORI_F_IDLENESS_GIVEN, M.MORI_F_SSD_TIER, M.MORI_F_SSD_TIER | M.MORI_F_SKIP_FIT, 0]
+        for step, flags in enumerate(forms):
+            if not flags & M.MORI_F_SSD_TIER and (pair.tier == 3).any():
+                flags |= M.MORI_F_SSD_TIER  # programs on the SSD tier need the three-tier policy
+                flags &= ~M.MORI_F_INCREMENTAL
+            kw = dict(gpu_bytes=int(rng.integers(0, inst.geom.num_blocks + 1)) * bb,
+                      cpu_bytes=int(rng.integers(0, nb_total + 1)) * bb, flags=flags,
+                      mode=(M.MORI_COPY_KERNEL, M.MORI_COPY_CE)[step % 2])
+            if flags & M.MORI_F_SSD_TIER:
+                kw["ssd_bytes"] = int(rng.integers(0, nb_total + 1)) * bb
+            if flags & M.MORI_F_IDLENESS_GIVEN:
+                kw["iota"] = rng.random(inst.P).astype(np.float32)
+            else:
+                kw["window"] = inst.window if step % 2 == 0 else inst.window[:, :, ::-1].copy()
+            if flags & M.MORI_F_INCREMENTAL:
+                kw["status"] = status
+            log(f"policy change seed={seed} step={step} flags={flags}")
+            res, plan = pair.step(**kw)
+            assert res.rc == oracle.OK, (seed, step, flags, res.rc)
+            status = np.where((status == 2) & (pair.tier != 2), 0, status).astype(np.uint8)
+    finally:
+        pair.close()
