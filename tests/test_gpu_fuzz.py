@@ -5,7 +5,9 @@ fragmentation, random budgets, both copy modes and small staging buffers
 (many chunks), several steps per pool, all through the C ABI and compared
 element by element (plan, tables, tiers, free map, every resident and host
 byte).  Then eviction orders at sizes on both sides of the switch between the
-one-kernel and the three-kernel radix passes."""
+one-kernel and the three-kernel radix passes, pools whose policy changes from
+step to step, and pools of 700-4096 programs (the rank kernel's radix-sort
+shapes) with windows of 1 to 64 cycles."""
 import numpy as np
 import pytest
 import torch
@@ -132,3 +134,38 @@ def test_policy_changes_between_steps(seed):
             status = np.where((status == 2) & (pair.tier != 2), 0, status).astype(np.uint8)
     finally:
         pair.close()
+
+
+@pytest.mark.parametrize("block", range(2))
+def test_random_large_program_counts(block):
+    """24 pools per block of 700-4096 programs (the rank kernel's larger
+    shapes) with windows of 1 to 64 cycles, every policy form, two steps each."""
+    for seed in range(block * 24, block * 24 + 24):
+        rng = np.random.default_rng(90000 + seed)
+        name, flags, tier_p = _policy(rng)
+        P = int(rng.choice([700, 1024, 1025, 3000, 4096]))
+        k = int(rng.choice([1, 5, 17, 64]))
+        inst = random_instance(rng, P=P, max_blocks=int(rng.choice([1, 3, 6])), geom=Geometry(1, 2, 1, 16, 0),
+                               tier_p=tier_p, ties=bool(rng.random() < 0.5), extra_free=int(rng.integers(1, 200)))
+        inst.window = rng.choice(np.array([0.0, 0.25, 0.5, 1.0, 3.0, 60.0], np.float32), size=(P, k, 2))
+        log(f"fuzz large seed={seed} {name} flags={flags} P={P} k={k} NB={inst.geom.num_blocks}")
+        pair = Pair(inst, seed=seed)
+        try:
+            bb = inst.geom.block_bytes
+            nb_total = inst.total_bytes // bb
+            status = rng.integers(0, 3 if name == "incremental" else 2, P).astype(np.uint8)
+            for step in range(2):
+                kw = dict(gpu_bytes=int(rng.integers(0, inst.geom.num_blocks + 1)) * bb,
+                          cpu_bytes=int(rng.integers(0, nb_total + 2)) * bb, flags=flags,
+                          ssd_bytes=int(rng.integers(0, nb_total + 2)) * bb if name == "ssd" else 0,
+                          mode=(M.MORI_COPY_KERNEL, M.MORI_COPY_CE)[(seed + step) % 2])
+                if name == "given":
+                    kw["iota"] = rng.random(P).astype(np.float32)
+                else:
+                    kw["window"] = inst.window if step == 0 else inst.window[:, :, ::-1].copy()
+                if flags & (M.MORI_F_STATUS_KEY | M.MORI_F_INCREMENTAL):
+                    kw["status"] = status
+                res, plan = pair.step(**kw)
+                assert res.rc == oracle.OK, (seed, step, res.rc)
+        finally:
+            pair.close()
