@@ -24,6 +24,7 @@
 // P <= 4096 programs fit in LDS (4 keys per thread), so the whole step is one
 // launch of a few microseconds; nothing here is bandwidth-bound.
 #include "mori_internal.h"
+#include "wave.h"
 
 namespace mori {
 namespace {
@@ -36,37 +37,6 @@ constexpr int RADIX_BITS = 8;
 constexpr int RADIX = 1 << RADIX_BITS;
 constexpr int KEY_BITS = 64;
 constexpr int GROUP_SHIFT = 61;  // incremental keys: listing group in the top three bits
-// Exclusive scan of one value per thread over the whole workgroup of NW
-// waves (thread order); *total receives the sum.  s_wave needs NW + 1 entries.
-template <int NW, typename T>
-__device__ T block_scan_excl(T v, T* s_wave, T* total) {
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  T x = v;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    T y = __shfl_up(x, off, 64);
-    if (lane >= off) x += y;
-  }
-  if (lane == 63) s_wave[wid] = x;
-  __syncthreads();
-  if (wid == 0) {
-    T w = lane < NW ? s_wave[lane] : T(0);
-    T wi = w;
-#pragma unroll
-    for (int off = 1; off < NW; off <<= 1) {
-      T y = __shfl_up(wi, off, 64);
-      if (lane >= off) wi += y;
-    }
-    if (lane < NW) s_wave[lane] = wi - w;
-    if (lane == NW - 1) s_wave[NW] = wi;
-  }
-  __syncthreads();
-  T res = s_wave[wid] + x - v;
-  *total = s_wave[NW];
-  __syncthreads();
-  return res;
-}
-
 // Exclusive scans of the IPT x RT items in rank order (item it of thread tid
 // has rank it * RT + tid), N values per item side by side: wave scans, the
 // per-(slice, wave) totals scanned by the first wave, and three barriers in
@@ -83,12 +53,7 @@ __device__ void scan_slices(const uint64_t (&v)[IPT][N], uint64_t (&ex)[IPT][N],
   for (int it = 0; it < IPT; ++it)
 #pragma unroll
     for (int n = 0; n < N; ++n) {
-      uint64_t x = v[it][n];
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const uint64_t y = __shfl_up(x, off, 64);
-        if (lane >= off) x += y;
-      }
+      const uint64_t x = wave::incl_add(v[it][n]);
       inc[it][n] = x;
       if (lane == 63) s_tot[(it * NW + wid) * N + n] = x;
     }
@@ -97,12 +62,7 @@ __device__ void scan_slices(const uint64_t (&v)[IPT][N], uint64_t (&ex)[IPT][N],
 #pragma unroll
     for (int n = 0; n < N; ++n) {
       const uint64_t w = lane < NS ? s_tot[lane * N + n] : 0ull;
-      uint64_t wi = w;
-#pragma unroll
-      for (int off = 1; off < NS; off <<= 1) {
-        const uint64_t y = __shfl_up(wi, off, 64);
-        if (lane >= off) wi += y;
-      }
+      const uint64_t wi = wave::incl_add(w);
       if (lane < NS) s_tot[lane * N + n] = wi - w;
       if (lane == NS - 1) s_tot[NS * N + n] = wi;
     }
@@ -115,6 +75,17 @@ __device__ void scan_slices(const uint64_t (&v)[IPT][N], uint64_t (&ex)[IPT][N],
 #pragma unroll
   for (int n = 0; n < N; ++n) total[n] = s_tot[NS * N + n];
   __syncthreads();
+}
+
+// Adds every thread's v into an LDS total with one atomic per wavefront (the
+// wave's sum by DPP); every thread of the workgroup calls it.
+__device__ inline void add_to(uint32_t* dst, uint32_t v) {
+  const uint32_t t = wave::sum(v);
+  if ((threadIdx.x & 63) == 0 && t) atomicAdd(dst, t);
+}
+__device__ inline void add_to(unsigned long long* dst, uint64_t v) {
+  const uint64_t t = wave::sum(v);
+  if ((threadIdx.x & 63) == 0 && t) atomicAdd(dst, (unsigned long long)t);
 }
 
 // Transition category.  Leaving the GPU for a tier that keeps the KV (CPU,
@@ -274,9 +245,16 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     k_or |= k;
     k_and &= k;
   }
-  if (k_or) atomicOr(&s_or, k_or);
-  if (k_and != ~0ull) atomicAnd(&s_and, k_and);
+  {
+    const uint64_t w_or = wave::all_or<uint64_t>(k_or), w_and = wave::all_and<uint64_t>(k_and);
+    if (lane == 0 && w_or) atomicOr(&s_or, (unsigned long long)w_or);
+    if (lane == 0 && w_and != ~0ull) atomicAnd(&s_and, (unsigned long long)w_and);
+  }
   if (err) atomicOr(&s_err, err);
+  if constexpr (!(IPT == 1 && RT <= 256)) {  // the first radix pass's digit counters
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) s_cnt[cidx(j * RT + tid)] = 0;
+  }
   __syncthreads();
   if (s_err) {
     if (tid == 0) {
@@ -300,11 +278,17 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     __syncthreads();
     uint32_t rank = tid;  // padding keeps its slot: every real rank is below P
     if ((uint32_t)tid < P) {
+      // eight keys' loads in flight per step; the padding keys past P (all
+      // ones, above every real key) count for nobody
       const uint64_t k = key[0];
+      const uint32_t P8 = (P + 7u) & ~7u;
       rank = 0;
-      for (uint32_t j = 0; j < P; ++j) {
-        const uint64_t kj = s_key[j];
-        rank += (kj < k) | ((kj == k) & (j < (uint32_t)tid));
+      for (uint32_t j0 = 0; j0 < P8; j0 += 8) {
+        uint64_t kj[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) kj[u] = s_key[j0 + u];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) rank += (kj[u] < k) | ((kj[u] == k) & (j0 + u < (uint32_t)tid));
       }
     }
     __syncthreads();
@@ -320,14 +304,13 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     // them in index order gives every (digit, item slice, wave) its output
     // base in (digit, original position) order, i.e. a stable pass.  Digits
     // on which every real key agrees are skipped; padding keeps the tail.
+    // Five barriers a pass: counts, wave totals, bases, scatter, and the
+    // read-back that also clears the next pass's counters.
     const uint64_t varying = s_or ^ s_and;
     const uint64_t lanemask_lt = (1ull << lane) - 1ull;
     for (int shift = 0; shift < KEY_BITS; shift += RADIX_BITS) {
       if (((varying >> shift) & (RADIX - 1)) == 0) continue;
       uint32_t digit[IPT], lrank[IPT];
-#pragma unroll
-      for (int j = 0; j < CPT; ++j) s_cnt[cidx(j * RT + tid)] = 0;
-      __syncthreads();
 #pragma unroll
       for (int it = 0; it < IPT; ++it) {
         const uint32_t d = (uint32_t)(key[it] >> shift) & (RADIX - 1);
@@ -343,13 +326,18 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
         lrank[it] = r;
       }
       __syncthreads();
-      uint32_t loc[CPT], sum = 0, tot;
+      uint32_t loc[CPT], sum = 0;
 #pragma unroll
       for (int j = 0; j < CPT; ++j) {
         loc[j] = s_cnt[cidx(tid * CPT + j)];
         sum += loc[j];
       }
-      uint32_t base = block_scan_excl<NW, uint32_t>(sum, s_w32, &tot);
+      // this thread's base: its wave's exclusive scan plus the totals of the
+      // waves before it (lane w < wid reads wave w's total)
+      const uint32_t incl = wave::incl_add(sum);
+      if (lane == 63) s_w32[wid] = incl;
+      __syncthreads();
+      uint32_t base = incl - sum + wave::sum(lane < wid ? s_w32[lane] : 0u);
 #pragma unroll
       for (int j = 0; j < CPT; ++j) {
         s_cnt[cidx(tid * CPT + j)] = base;
@@ -368,6 +356,8 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
         key[it] = s_key[it * RT + tid];
         id[it] = s_id[it * RT + tid];
       }
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) s_cnt[cidx(j * RT + tid)] = 0;  // every base of this pass is read
       __syncthreads();
     }
   }
@@ -399,14 +389,18 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
   if (incremental) {
     // listing groups: [0, g1) GPU, [g1, g2) CPU, [g2, g3) Waiting returning,
     // [g3, g4) new arrivals, [g4, P) Waiting Acting
+    uint32_t gc[5] = {0, 0, 0, 0, 0}, cr = 0;
 #pragma unroll
     for (int it = 0; it < IPT; ++it) {
       const uint32_t r = it * RT + tid;
-      if (r >= P) continue;
-      const uint32_t g = (uint32_t)(key[it] >> GROUP_SHIFT);
-      atomicAdd(&s_grp[g], 1u);
-      if (g == MORI_TIER_CPU && !((key[it] >> 31) & 1u)) atomicAdd(&s_cpu_reasoning, 1u);
+      const uint32_t g = r < P ? (uint32_t)(key[it] >> GROUP_SHIFT) : 5u;
+#pragma unroll
+      for (int j = 0; j < 5; ++j) gc[j] += g == (uint32_t)j;
+      cr += g == MORI_TIER_CPU && !((key[it] >> 31) & 1u);
     }
+#pragma unroll
+    for (int j = 0; j < 5; ++j) add_to(&s_grp[j], gc[j]);
+    add_to(&s_cpu_reasoning, cr);
     __syncthreads();
     const uint32_t g1 = s_grp[0], g2 = g1 + s_grp[1], g3 = g2 + s_grp[2], g4 = g3 + s_grp[3];
     const uint64_t gpu_total = g1 ? s_key[g1 - 1] : 0;
@@ -420,8 +414,8 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
       if (r < g1 && S[it] <= a.gpu_bytes) ++kg;
       if (r >= g1 && r < g2 && S[it] - gpu_total <= a.cpu_bytes) ++kc;
     }
-    if (kg) atomicAdd(&s_k_gpu, kg);
-    if (kc) atomicAdd(&s_k_cpu, kc);
+    add_to(&s_k_gpu, kg);
+    add_to(&s_k_cpu, kc);
     __syncthreads();
     const uint32_t k_gpu = s_k_gpu, k_cpu = s_k_cpu;
     const uint64_t gpu_kept = k_gpu ? s_key[k_gpu - 1] : 0;
@@ -492,8 +486,8 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
       ng += s_tier[r] == MORI_TIER_GPU;
       nc += s_tier[r] == MORI_TIER_CPU;
     }
-    if (ng) atomicAdd(&s_m_gpu, ng);
-    if (nc) atomicAdd(&s_m_cpu, nc);
+    add_to(&s_m_gpu, ng);
+    add_to(&s_m_cpu, nc);
   } else if (!(a.flags & MORI_F_SKIP_FIT)) {
     // S is non-decreasing in rank order, so the longest feasible prefix is
     // the number of ranks whose inclusive prefix fits the budget.
@@ -501,7 +495,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
 #pragma unroll
     for (int it = 0; it < IPT; ++it)
       if (it * RT + tid < (int)P && S[it] <= a.gpu_bytes) ++c;
-    if (c) atomicAdd(&s_m_gpu, c);
+    add_to(&s_m_gpu, c);
     __syncthreads();
     const uint32_t m_gpu = s_m_gpu;
 #pragma unroll
@@ -515,7 +509,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
       const uint32_t r = it * RT + tid;
       if (r >= m_gpu && r < P && S[it] - gpu_part <= a.cpu_bytes) ++c;
     }
-    if (c) atomicAdd(&s_m_cpu, c);
+    add_to(&s_m_cpu, c);
     __syncthreads();
     const uint32_t m_cpu = s_m_cpu, upper = m_gpu + m_cpu;
     uint32_t m_ssd = 0;
@@ -531,7 +525,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
         const uint32_t r = it * RT + tid;
         if (r >= upper && r < P && S[it] - upper_part <= a.ssd_bytes) ++c;
       }
-      if (c) atomicAdd(&s_m_ssd, c);
+      add_to(&s_m_ssd, c);
       __syncthreads();
       m_ssd = s_m_ssd;
     }
@@ -578,7 +572,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
   // Global stores wait until after the last barrier: a barrier waits for the
   // stores still in flight, so stores issued earlier would stall every one.
   uint64_t vab[IPT][2], exab[IPT][2], totab[2];
-  uint8_t catv[IPT], toldv[IPT], tnewv[IPT];
+  uint8_t catv[IPT], tnewv[IPT];
   uint32_t n_dg = 0, n_dc = 0, n_ag = 0, n_ac = 0;
   uint64_t gpu_after = 0, cpu_after = 0, ssd_after = 0;
 #pragma unroll
@@ -591,7 +585,6 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
       const uint8_t told = s_told[p], tnew = s_tier[r];
       const uint8_t c = category(told, tnew);
       catv[it] = c;
-      toldv[it] = told;
       tnewv[it] = tnew;
       if (c == MORI_CAT_OUT) va = nb[it], vb = 1ull << 32;
       if (c == MORI_CAT_IN) va = (uint64_t)nb[it] << 32, vb = 1ull << 48;
@@ -611,16 +604,31 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
   const uint32_t pages_out = (uint32_t)(carryA & 0xFFFFFFFFu), pages_in = (uint32_t)(carryA >> 32);
   const uint32_t pages_admit = (uint32_t)(carryB & 0xFFFFFFFFu);
   const uint32_t n_out = (uint32_t)((carryB >> 32) & 0xFFFFu), n_in = (uint32_t)(carryB >> 48);
-  if (n_dg) atomicAdd(&s_n_drop_gpu, n_dg);
-  if (n_dc) atomicAdd(&s_n_drop_cpu, n_dc);
-  if (n_ag) atomicAdd(&s_n_admit_gpu, n_ag);
-  if (n_ac) atomicAdd(&s_n_admit_cpu, n_ac);
-  if (gpu_after) atomicAdd(&s_gpu_after, (unsigned long long)gpu_after);
-  if (cpu_after) atomicAdd(&s_cpu_after, (unsigned long long)cpu_after);
-  if (ssd_after) atomicAdd(&s_ssd_after, (unsigned long long)ssd_after);
+  // program-indexed staging, so the per-program stores below are coalesced:
+  // the new tier and the page base by program id (every read of the
+  // rank-indexed s_tier and s_nblk came before the scan's first barrier)
+#pragma unroll
+  for (int it = 0; it < IPT; ++it) {
+    const uint32_t r = it * RT + tid;
+    if (r >= P) continue;
+    const uint32_t p = id[it];
+    const uint64_t exA = exab[it][0], exB = exab[it][1];
+    s_tier[p] = tnewv[it];
+    if (catv[it] == MORI_CAT_OUT) s_nblk[p] = (uint32_t)(exA & 0xFFFFFFFFu);
+    if (catv[it] == MORI_CAT_IN) s_nblk[p] = (uint32_t)(exA >> 32);
+    if (catv[it] == MORI_CAT_ADMIT_GPU) s_nblk[p] = pages_in + (uint32_t)(exB & 0xFFFFFFFFu);
+  }
+  add_to(&s_n_drop_gpu, n_dg);
+  add_to(&s_n_drop_cpu, n_dc);
+  add_to(&s_n_admit_gpu, n_ag);
+  add_to(&s_n_admit_cpu, n_ac);
+  add_to(&s_gpu_after, gpu_after);
+  add_to(&s_cpu_after, cpu_after);
+  add_to(&s_ssd_after, ssd_after);
   __syncthreads();
 
   // ---- 5. the plan's stores ------------------------------------------------
+  // by rank: order, prefix and the swap lists
 #pragma unroll
   for (int it = 0; it < IPT; ++it) {
     const uint32_t r = it * RT + tid;
@@ -628,39 +636,40 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     const uint32_t p = id[it];
     a.order[r] = p;
     a.prefix[r] = S[it];
-    a.tier_old[p] = toldv[it];
-    a.tier_new[p] = tnewv[it];
-    a.cat[p] = catv[it];
     *host_mirror(a, a.order + r) = p;
     *host_mirror(a, a.prefix + r) = S[it];
-    *host_mirror(a, a.tier_old + p) = toldv[it];
-    *host_mirror(a, a.tier_new + p) = tnewv[it];
-    *host_mirror(a, a.cat + p) = catv[it];
     const uint64_t exA = exab[it][0], exB = exab[it][1];
-    const uint32_t pg_out_ex = (uint32_t)(exA & 0xFFFFFFFFu), pg_in_ex = (uint32_t)(exA >> 32);
-    const uint32_t pg_admit_ex = (uint32_t)(exB & 0xFFFFFFFFu);
     const uint32_t idx_out = (uint32_t)((exB >> 32) & 0xFFFFu), idx_in = (uint32_t)(exB >> 48);
-    switch (catv[it]) {
-      case MORI_CAT_OUT:
-        a.out_prog[idx_out] = p;
-        a.out_pg_base[idx_out] = pg_out_ex;
-        *host_mirror(a, a.out_prog + idx_out) = p;
-        *host_mirror(a, a.out_pg_base + idx_out) = pg_out_ex;
-        a.base[p] = pg_out_ex;
-        break;
-      case MORI_CAT_IN:  // programs promoted from the CPU (or SSD) tier take the first slots (Sec. 4.3.1)
-        a.in_prog[idx_in] = p;
-        a.in_pg_base[idx_in] = pg_in_ex;
-        *host_mirror(a, a.in_prog + idx_in) = p;
-        *host_mirror(a, a.in_pg_base + idx_in) = pg_in_ex;
-        a.base[p] = pg_in_ex;
-        break;
-      case MORI_CAT_ADMIT_GPU:  // then programs admitted from Waiting (priority (2))
-        a.base[p] = pages_in + pg_admit_ex;
-        break;
-      default:
-        break;
+    if (catv[it] == MORI_CAT_OUT) {
+      const uint32_t pg = (uint32_t)(exA & 0xFFFFFFFFu);
+      a.out_prog[idx_out] = p;
+      a.out_pg_base[idx_out] = pg;
+      *host_mirror(a, a.out_prog + idx_out) = p;
+      *host_mirror(a, a.out_pg_base + idx_out) = pg;
     }
+    if (catv[it] == MORI_CAT_IN) {  // programs promoted from the CPU (or SSD) tier take the first slots (Sec. 4.3.1)
+      const uint32_t pg = (uint32_t)(exA >> 32);
+      a.in_prog[idx_in] = p;
+      a.in_pg_base[idx_in] = pg;
+      *host_mirror(a, a.in_prog + idx_in) = p;
+      *host_mirror(a, a.in_pg_base + idx_in) = pg;
+    }
+  }
+  // by program id: tiers, categories and the page bases (swap-outs from their
+  // first released page, swap-ins from theirs, then the programs admitted from
+  // Waiting after every swap-in: priority (2))
+#pragma unroll
+  for (int it = 0; it < IPT; ++it) {
+    const uint32_t x = it * RT + tid;
+    if (x >= P) continue;
+    const uint8_t told = s_told[x], tnew = s_tier[x], c = category(told, tnew);
+    a.tier_old[x] = told;
+    a.tier_new[x] = tnew;
+    a.cat[x] = c;
+    *host_mirror(a, a.tier_old + x) = told;
+    *host_mirror(a, a.tier_new + x) = tnew;
+    *host_mirror(a, a.cat + x) = c;
+    if (c == MORI_CAT_OUT || c == MORI_CAT_IN || c == MORI_CAT_ADMIT_GPU) a.base[x] = s_nblk[x];
   }
   if (tid == 0) {
     a.out_pg_base[n_out] = pages_out;
