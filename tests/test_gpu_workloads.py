@@ -94,7 +94,7 @@ class Harness:
                             torch.from_numpy(oi).cuda(), pages=torch.from_numpy(pages).cuda())
         for p in np.flatnonzero(((cat == oracle.ADMIT_CPU) | (cat == oracle.ADMIT_SSD)) & (inst.nblk > 0)):
             dst = torch.from_numpy(self.tp.host_view(int(p)).view(np.int16))
-            dst.copy_(program_content_torch(inst, self.bank_dev, int(p)).cpu())
+            program_content_torch(inst, self.bank_dev, int(p), out=dst)  # one copy into the pinned tier
         torch.cuda.synchronize()
 
     def check_tags(self):
