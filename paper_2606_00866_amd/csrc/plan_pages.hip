@@ -9,8 +9,11 @@
 //   count    per 1024-page tile: pages free before the step, released pages
 //            of dropped programs, released pages of swapped-out programs; a
 //            page that is neither free nor owned is a leak;
-//   scan     one workgroup: exclusive prefix over tiles, totals, capacity;
-//            the summary is final here and is stored into the host mirror;
+//   scan     exclusive prefix over tiles, totals, capacity; the summary is
+//            final here and is stored into the host mirror.  Up to
+//            SCAN_IN_ASSIGN tiles every assign workgroup does this itself
+//            from the tile counts (one launch fewer); above, one workgroup
+//            of a kernel of its own;
 //   assign   slot j of the incoming programs takes the j-th page of
 //            (free-before ++ dropped ++ swapped out, each ascending): pages
 //            nothing reads come before pages the swap-out reads, so the
@@ -24,11 +27,13 @@
 // leaves the caller's state untouched.  All loops are grid-stride over sizes
 // the host knows (tbl_len, num_blocks), bounded by device values read once.
 #include "mori_internal.h"
+#include "wave.h"
 
 namespace mori {
 namespace {
 
 constexpr int WG = 256;
+constexpr uint32_t SCAN_IN_ASSIGN = 1024;  // tiles (2^20 pages): each assign workgroup reads 16 B per tile
 
 // Largest p in [0, P) with off[p] <= e (so off[p] <= e < off[p+1] when e < off[P]).
 __device__ inline uint32_t find_program(const uint32_t* off, uint32_t P, uint32_t e) {
@@ -87,9 +92,12 @@ __global__ __launch_bounds__(WG) void pages_count_kernel(PlanArgs a) {
     else if (st & PS_REL) ++nd;
     else if (st == 0) err |= MORI_DEV_PAGE_LEAK;
   }
-  if (nf) atomicAdd(&s_free, nf);
-  if (nd) atomicAdd(&s_drop, nd);
-  if (nc) atomicAdd(&s_copy, nc);
+  const uint32_t wf = wave::sum(nf), wd = wave::sum(nd), wc = wave::sum(nc);  // one LDS atomic per wavefront
+  if ((threadIdx.x & 63) == 0) {
+    if (wf) atomicAdd(&s_free, wf);
+    if (wd) atomicAdd(&s_drop, wd);
+    if (wc) atomicAdd(&s_copy, wc);
+  }
   if (err) atomicOr(&s_err, err);
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -104,22 +112,12 @@ template <int WGS>
 __device__ uint64_t wg_scan_excl(uint64_t v, uint64_t* s_wave, uint64_t* total) {
   constexpr int NWV = WGS / 64;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  uint64_t x = v;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const uint64_t y = __shfl_up(x, off, 64);
-    if (lane >= off) x += y;
-  }
+  const uint64_t x = wave::incl_add(v);
   if (lane == 63) s_wave[wid] = x;
   __syncthreads();
   if (wid == 0) {
     const uint64_t w = lane < NWV ? s_wave[lane] : 0ull;
-    uint64_t wi = w;
-#pragma unroll
-    for (int off = 1; off < NWV; off <<= 1) {
-      const uint64_t y = __shfl_up(wi, off, 64);
-      if (lane >= off) wi += y;
-    }
+    const uint64_t wi = wave::incl_add(w);
     if (lane < NWV) s_wave[lane] = wi - w;
     if (lane == NWV - 1) s_wave[NWV] = wi;
   }
@@ -128,6 +126,22 @@ __device__ uint64_t wg_scan_excl(uint64_t v, uint64_t* s_wave, uint64_t* total) 
   *total = s_wave[NWV];
   __syncthreads();
   return res;
+}
+
+// The page totals into the summary, the capacity check, and the summary into
+// the host mirror (final from here).  One thread.
+__device__ void finish_summary(const PlanArgs& a, uint64_t nf, uint64_t nd, uint64_t nc) {
+  DevSummary* s = a.sum;
+  s->pages_free_before = nf;
+  s->pages_released = nd + nc;
+  s->pages_dropped = nd;
+  if (s->need > nf + nd + nc) {
+    atomicOr(&s->error, MORI_DEV_NOSPC);
+  } else {
+    s->pages_recycled = s->need > nf ? s->need - nf : 0;
+    s->pages_free_after = nf + nd + nc - s->need;
+  }
+  *host_mirror(a, s) = *s;
 }
 
 __global__ __launch_bounds__(1024) void pages_scan_kernel(PlanArgs a) {
@@ -149,25 +163,54 @@ __global__ __launch_bounds__(1024) void pages_scan_kernel(PlanArgs a) {
       carry[half] += tot;
     }
   }
-  if (threadIdx.x == 0) {
-    DevSummary* s = a.sum;
-    const uint64_t nf = carry[0] & 0xFFFFFFFFull, nd = carry[0] >> 32, nc = carry[1];
-    s->pages_free_before = nf;
-    s->pages_released = nd + nc;
-    s->pages_dropped = nd;
-    if (s->need > nf + nd + nc) {
-      atomicOr(&s->error, MORI_DEV_NOSPC);
-    } else {
-      s->pages_recycled = s->need > nf ? s->need - nf : 0;
-      s->pages_free_after = nf + nd + nc - s->need;
-    }
-    *host_mirror(a, s) = *s;  // the summary is final from here
-  }
+  if (threadIdx.x == 0) finish_summary(a, carry[0] & 0xFFFFFFFFull, carry[0] >> 32, carry[1]);
 }
 
+// SCAN: the tile scan is done here (every workgroup scans the counts of the
+// tiles before its own and totals all of them; workgroup 0 finishes the
+// summary), else it comes from pages_scan_kernel.
+template <bool SCAN>
 __global__ __launch_bounds__(WG) void pages_assign_kernel(PlanArgs a) {
   __shared__ uint64_t s_wave[WG / 64 + 1];
-  if (a.sum->error) return;
+  __shared__ uint64_t s_red[WG / 64][4];
+  if (a.sum->error) {
+    if (SCAN && blockIdx.x == 0 && threadIdx.x == 0) *host_mirror(a, a.sum) = *a.sum;
+    return;
+  }
+  const uint64_t need = a.sum->need;
+  uint64_t tb, tbc, nf_all, nd_all;
+  if constexpr (SCAN) {
+    uint64_t v[4] = {0, 0, 0, 0};  // prefix (free | dropped << 32), prefix swapped-out, and the totals
+    for (uint32_t t = threadIdx.x; t < a.ntiles; t += WG) {
+      const uint64_t c0 = a.tile_cnt[t], c1 = a.tile_cnt[a.ntiles + t];
+      if (t < blockIdx.x) v[0] += c0, v[1] += c1;
+      v[2] += c0;
+      v[3] += c1;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint64_t w = wave::sum(v[k]);
+      if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6][k] = w;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      v[k] = 0;
+#pragma unroll
+      for (int w = 0; w < WG / 64; ++w) v[k] += s_red[w][k];
+    }
+    tb = v[0];
+    tbc = v[1];
+    nf_all = v[2] & 0xFFFFFFFFull;
+    nd_all = v[2] >> 32;
+    if (blockIdx.x == 0 && threadIdx.x == 0) finish_summary(a, nf_all, nd_all, v[3]);
+    if (need > nf_all + nd_all + v[3]) return;  // no room: workgroup 0 sets the error
+  } else {
+    tb = a.tile_base[blockIdx.x];
+    tbc = a.tile_base[a.ntiles + blockIdx.x];
+    nf_all = a.sum->pages_free_before;
+    nd_all = a.sum->pages_dropped;
+  }
   const uint32_t per = PAGE_TILE / WG;
   const uint64_t start = (uint64_t)blockIdx.x * PAGE_TILE + (uint64_t)threadIdx.x * per;
   uint32_t st[PAGE_TILE / WG];
@@ -183,11 +226,9 @@ __global__ __launch_bounds__(WG) void pages_assign_kernel(PlanArgs a) {
   uint64_t tot;
   const uint64_t ex = wg_scan_excl<WG>((uint64_t)nf | ((uint64_t)nd << 32), s_wave, &tot);
   const uint64_t exc = wg_scan_excl<WG>(nc, s_wave, &tot);
-  const uint64_t tb = a.tile_base[blockIdx.x], tbc = a.tile_base[a.ntiles + blockIdx.x];
   uint64_t fi = (tb & 0xFFFFFFFFull) + (ex & 0xFFFFFFFFull);
   uint64_t di = (tb >> 32) + (ex >> 32);
   uint64_t ci = tbc + exc;
-  const uint64_t nf_all = a.sum->pages_free_before, nd_all = a.sum->pages_dropped, need = a.sum->need;
 #pragma unroll
   for (uint32_t j = 0; j < per; ++j) {
     const uint64_t pg = start + j;
@@ -260,9 +301,13 @@ inline uint32_t grid_for(uint64_t n, uint32_t cap) {
 hipError_t launch_pages(const PlanArgs& a, hipStream_t s) {
   const uint32_t ge = grid_for(a.tbl_len > a.P ? a.tbl_len : a.P, 2048);
   hipLaunchKernelGGL(pages_claim_kernel, dim3(ge), dim3(WG), 0, s, a);
-  if (a.ntiles) hipLaunchKernelGGL(pages_count_kernel, dim3(a.ntiles), dim3(WG), 0, s, a);
-  hipLaunchKernelGGL(pages_scan_kernel, dim3(1), dim3(1024), 0, s, a);
-  if (a.ntiles) hipLaunchKernelGGL(pages_assign_kernel, dim3(a.ntiles), dim3(WG), 0, s, a);
+  hipLaunchKernelGGL(pages_count_kernel, dim3(a.ntiles), dim3(WG), 0, s, a);  // ntiles >= 1: the pool has a page
+  if (a.ntiles <= SCAN_IN_ASSIGN) {
+    hipLaunchKernelGGL(pages_assign_kernel<true>, dim3(a.ntiles), dim3(WG), 0, s, a);
+  } else {
+    hipLaunchKernelGGL(pages_scan_kernel, dim3(1), dim3(1024), 0, s, a);
+    hipLaunchKernelGGL(pages_assign_kernel<false>, dim3(a.ntiles), dim3(WG), 0, s, a);
+  }
   hipLaunchKernelGGL(commit_kernel, dim3(ge), dim3(WG), 0, s, a);
   return hipGetLastError();
 }

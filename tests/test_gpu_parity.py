@@ -530,3 +530,37 @@ def test_two_contexts_on_two_host_threads():
     finally:
         for pair in pairs:
             pair.close()
+
+
+@pytest.mark.parametrize("target", [1 << 20, (1 << 20) + 1, 1_500_000])
+def test_pools_around_the_tile_scan_switch(target):
+    """Pools of 2^20 pages (1024 tiles of 1024 pages: each page-assignment
+    workgroup scans the tile counts itself), one page more (1025 tiles: the
+    tile scan is a kernel of its own) and 1.5 M pages, about 85% of them owned,
+    so free pages, released pages and incoming slots span many tiles and
+    swap-ins land on pages the same step releases: plan, tables, free map and
+    bytes equal the oracle's, two steps each."""
+    geom = Geometry(layers=1, planes=1, block_tokens=1, row_bytes=16, num_blocks=0)
+    P, tier_p = 300, (0.45, 0.35, 0.2)
+    max_blocks = int(2 * 0.85 * target / (P * tier_p[0]))
+    gpu_blocks = random_instance(np.random.default_rng(target), P=P, max_blocks=max_blocks, geom=geom, tier_p=tier_p,
+                                 extra_free=0).geom.num_blocks
+    assert gpu_blocks < target
+    inst = random_instance(np.random.default_rng(target), P=P, max_blocks=max_blocks, geom=geom, tier_p=tier_p,
+                           extra_free=target - gpu_blocks)
+    assert inst.geom.num_blocks == target
+    log(f"tile scan switch: NB={target} P={inst.P} owned={gpu_blocks} blocks={int(inst.nblk.sum())}")
+    pair = Pair(inst, seed=target % 1000)
+    try:
+        bb = inst.geom.block_bytes
+        recycled = 0
+        for step in range(2):
+            w = inst.window if step == 0 else inst.window[:, :, ::-1].copy()
+            res, plan = pair.step(gpu_bytes=min(inst.total_bytes // 2 // bb, target) * bb,
+                                  cpu_bytes=int(inst.total_bytes * 0.3) // bb * bb, window=w,
+                                  mode=(M.MORI_COPY_KERNEL, M.MORI_COPY_CE)[step])
+            assert res.rc == oracle.OK and plan.n_in + plan.n_out > 0
+            recycled += plan.pages_recycled
+        assert recycled > 0
+    finally:
+        pair.close()
