@@ -45,6 +45,7 @@
 // Everything is latency-bound at 10^5-10^6 blocks (tens of microseconds);
 // the workspace is the caller's, so nothing is allocated here.
 #include "mori_internal.h"
+#include "wave.h"
 
 namespace mori {
 namespace {
@@ -58,6 +59,7 @@ constexpr uint32_t SMALL_SORT = 1u << 19;
 inline int keys_per_thread(uint32_t N) { return N <= SMALL_SORT ? 4 : 8; }
 constexpr uint64_t TIME_LIMIT = 1ull << 62;
 constexpr uint32_t KEY_WG_MAX = 128;     // workgroups of the keys kernel at most (one digit-count set each)
+constexpr int KEYS_PER_ROUND = 4;        // keys per thread whose loads the keys kernel issues together
 constexpr uint32_t TOT_SPLIT = 8;        // totals: workgroups per pass, each summing a share of the sets
 // Tile counts up to this use one look-back kernel per pass, more use three
 // kernels (histogram, per-digit scan, scatter): each look-back round is a
@@ -115,39 +117,64 @@ __global__ __launch_bounds__(ET) void evict_keys_kernel(EvictArgs a) {
   for (int k = 0; k < 8; ++k) s_c[k][threadIdx.x] = 0;
   __syncthreads();
   uint64_t o = 0, n = ~0ull, err = 0;
+  const int lane = threadIdx.x & 63;
+  // rounds of KEYS_PER_ROUND keys per thread, all their loads issued first;
   // uniform trip count: the cross-lane steps below need every lane of the wave
-  for (uint64_t i0 = (uint64_t)blockIdx.x * ET; i0 < a.N; i0 += (uint64_t)gridDim.x * ET) {
-    const uint64_t i = i0 + threadIdx.x;
-    bool valid = i < a.N;
-    uint64_t key = 0;
-    if (valid) {
-      const uint8_t t = a.type[i];
-      const uint64_t la = a.last_access[i];
-      if (t > MORI_TYPE_INACTIVE || la >= TIME_LIMIT) {
-        err |= MORI_DEV_BAD_BLOCK;
-        valid = false;
-      } else {
-        key = ((uint64_t)pos[t] << 62) | la;
-        a.keys[0][i] = key;
-        a.vals[0][i] = (uint32_t)i;
-        o |= key;
-        n &= key;
-      }
-    }
-    if (!a.onesweep) continue;  // uniform: the three-kernel passes count per tile
-    // runs of equal keys within the wave (the blocks of a program share their
-    // time): the first lane of a run adds the run's length for each digit
-    const int lane = threadIdx.x & 63;
-    const uint64_t prev = __shfl_up(key, 1, 64);
-    const bool prev_valid = __shfl_up(valid ? 1 : 0, 1, 64) != 0;
-    const bool head = valid && (lane == 0 || !prev_valid || prev != key);
-    const uint64_t heads = __ballot(head);
-    const uint64_t ends = heads | ~__ballot(valid);  // a run ends at the next head or invalid lane
-    if (head) {
-      const uint64_t later = lane == 63 ? 0ull : ends & ~((2ull << lane) - 1ull);
-      const uint32_t len = (later ? (uint32_t)__builtin_ctzll(later) : 64u) - (uint32_t)lane;
+  for (uint64_t i0 = (uint64_t)blockIdx.x * ET * KEYS_PER_ROUND; i0 < a.N;
+       i0 += (uint64_t)gridDim.x * ET * KEYS_PER_ROUND) {
+    uint8_t typ[KEYS_PER_ROUND];
+    uint64_t la[KEYS_PER_ROUND];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) atomicAdd(&s_c[k][(uint32_t)(key >> (8 * k)) & 255u], len);
+    for (int u = 0; u < KEYS_PER_ROUND; ++u) {
+      const uint64_t i = i0 + (uint64_t)u * ET + threadIdx.x;
+      typ[u] = i < a.N ? a.type[i] : 0;
+      la[u] = i < a.N ? a.last_access[i] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < KEYS_PER_ROUND; ++u) {
+      const uint64_t i = i0 + (uint64_t)u * ET + threadIdx.x;
+      bool valid = i < a.N;
+      uint64_t key = 0;
+      if (valid) {
+        if (typ[u] > MORI_TYPE_INACTIVE || la[u] >= TIME_LIMIT) {
+          err |= MORI_DEV_BAD_BLOCK;
+          valid = false;
+        } else {
+          key = ((uint64_t)pos[typ[u]] << 62) | la[u];
+          a.keys[0][i] = key;
+          a.vals[0][i] = (uint32_t)i;
+          o |= key;
+          n &= key;
+        }
+      }
+      if (!a.onesweep) continue;  // uniform: the three-kernel passes count per tile
+      // runs of equal keys within the wave (the blocks of a program share their
+      // time): the first lane of a run adds the run's length for each digit
+      const uint64_t prev = __shfl_up(key, 1, 64);
+      const bool prev_valid = __shfl_up(valid ? 1 : 0, 1, 64) != 0;
+      const bool head = valid && (lane == 0 || !prev_valid || prev != key);
+      const uint64_t heads = __ballot(head);
+      const uint64_t vmask = __ballot(valid);
+      if (!heads) continue;  // uniform: no valid key in this wave
+      const uint64_t ends = heads | ~vmask;  // a run ends at the next head or invalid lane
+      uint32_t len = 0;
+      if (head) {
+        const uint64_t later = lane == 63 ? 0ull : ends & ~((2ull << lane) - 1ull);
+        len = (later ? (uint32_t)__builtin_ctzll(later) : 64u) - (uint32_t)lane;
+      }
+      // a digit that every run of the wave shares (the high time digits and
+      // the type, mostly) takes one increment of all the wave's valid keys
+      const int first = __builtin_ctzll(heads);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const uint32_t d = (uint32_t)(key >> (8 * k)) & 255u;
+        const uint32_t d0 = (uint32_t)__builtin_amdgcn_readlane((int)d, first);
+        if (__ballot(head && d != d0) == 0) {
+          if (lane == first) atomicAdd(&s_c[k][d0], (uint32_t)__popcll(vmask));
+        } else if (head) {
+          atomicAdd(&s_c[k][d], len);
+        }
+      }
     }
   }
   __syncthreads();
@@ -156,11 +183,9 @@ __global__ __launch_bounds__(ET) void evict_keys_kernel(EvictArgs a) {
     for (int k = 0; k < 8; ++k) a.part[((uint64_t)blockIdx.x * 8 + k) * 256 + threadIdx.x] = s_c[k][threadIdx.x];
   // wave, then workgroup reduction: one set of global atomics per workgroup
   __shared__ uint64_t s_red[3][ENW];
-  for (int off = 32; off > 0; off >>= 1) {
-    o |= __shfl_xor(o, off, 64);
-    n &= __shfl_xor(n, off, 64);
-    err |= __shfl_xor(err, off, 64);
-  }
+  o = wave::all_or<uint64_t>(o);
+  n = wave::all_and<uint64_t>(n);
+  err = wave::all_or<uint64_t>(err);
   const int wid = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) {
     s_red[0][wid] = o;
@@ -226,12 +251,7 @@ __global__ __launch_bounds__(ET) void evict_hist_kernel(EvictArgs a, int shift) 
 // Block-wide exclusive scan of one u32 per thread (256 threads); *total gets the sum.
 __device__ inline uint32_t scan256(uint32_t v, uint32_t* s_w, uint32_t* total) {
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  uint32_t x = v;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const uint32_t y = __shfl_up(x, off, 64);
-    if (lane >= off) x += y;
-  }
+  const uint32_t x = wave::incl_add(v);
   if (lane == 63) s_w[wid] = x;
   __syncthreads();
   uint32_t before = 0, all = 0;
@@ -503,12 +523,7 @@ __global__ __launch_bounds__(ET) void evict_prefix_tiles_kernel(EvictArgs a) {
   }
   // exclusive scan of the per-thread totals
   const int lane = tid & 63, wid = tid >> 6;
-  uint64_t x = sum;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const uint64_t y = __shfl_up(x, off, 64);
-    if (lane >= off) x += y;
-  }
+  const uint64_t x = wave::incl_add(sum);
   if (lane == 63) s_w[wid] = x;
   __syncthreads();
   if (tid == 0) {
@@ -541,22 +556,12 @@ __global__ __launch_bounds__(1024) void evict_prefix_top_kernel(EvictArgs a) {
   for (uint32_t t0 = 0; t0 < a.ntiles; t0 += 1024) {
     const uint32_t t = t0 + threadIdx.x;
     const uint64_t v = t < a.ntiles ? a.tile_sum[t] : 0ull;
-    uint64_t x = v;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const uint64_t y = __shfl_up(x, off, 64);
-      if (lane >= off) x += y;
-    }
+    const uint64_t x = wave::incl_add(v);
     if (lane == 63) s_w[wid] = x;
     __syncthreads();
     if (wid == 0) {
       const uint64_t w = lane < 16 ? s_w[lane] : 0ull;
-      uint64_t wi = w;
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) {
-        const uint64_t y = __shfl_up(wi, off, 64);
-        if (lane >= off) wi += y;
-      }
+      const uint64_t wi = wave::incl_add(w);
       if (lane < 16) s_w[lane] = wi - w;
       if (lane == 15) s_w[16] = wi;
     }
@@ -582,7 +587,7 @@ __global__ __launch_bounds__(ET) void evict_prefix_fix_kernel(EvictArgs a) {
     }
   }
   __shared__ uint32_t s_short[ENW];
-  for (int off = 32; off > 0; off >>= 1) short_of_need += __shfl_xor(short_of_need, off, 64);
+  short_of_need = wave::sum(short_of_need);
   if ((threadIdx.x & 63) == 0) s_short[threadIdx.x >> 6] = short_of_need;
   __syncthreads();
   if (threadIdx.x == 0) {
