@@ -236,12 +236,7 @@ __global__ __launch_bounds__(ET) void evict_hist_kernel(EvictArgs a, int shift) 
     const uint64_t i = base + it * ET + threadIdx.x;
     const bool valid = i < a.N;
     const uint32_t d = valid ? (uint32_t)(k[i] >> shift) & 255u : 0u;
-    uint64_t same = __ballot(valid);
-#pragma unroll
-    for (int b = 0; b < 8; ++b) {
-      const uint64_t bal = __ballot((d >> b) & 1u);
-      same &= ((d >> b) & 1u) ? bal : ~bal;
-    }
+    const uint64_t same = __ballot(valid) & ~wave::digit_differs<8>(d);
     if (valid && (same & lanemask_lt) == 0) atomicAdd(&s_h[d], (uint32_t)__popcll(same));
   }
   __syncthreads();
@@ -319,12 +314,7 @@ __global__ __launch_bounds__(ET) void evict_scatter_kernel(EvictArgs a, int shif
     key[it] = valid ? ks[i] : 0ull;
     val[it] = valid ? vs[i] : 0u;
     const uint32_t d = (uint32_t)(key[it] >> shift) & 255u;
-    uint64_t same = __ballot(valid);
-#pragma unroll
-    for (int b = 0; b < 8; ++b) {
-      const uint64_t bal = __ballot((d >> b) & 1u);
-      same &= ((d >> b) & 1u) ? bal : ~bal;
-    }
+    const uint64_t same = __ballot(valid) & ~wave::digit_differs<8>(d);
     const uint32_t r = __popcll(same & lanemask_lt);
     if (valid && r == 0) s_cnt[it][wid][d] = (uint16_t)__popcll(same);
     dig[it] = valid ? d : 256u;
@@ -409,12 +399,7 @@ __global__ __launch_bounds__(ET) void evict_pass_kernel(EvictArgs a, int shift) 
     key[it] = valid ? ks[i] : 0ull;
     val[it] = valid ? vs[i] : 0u;
     const uint32_t d = (uint32_t)(key[it] >> shift) & 255u;
-    uint64_t same = __ballot(valid);
-#pragma unroll
-    for (int b = 0; b < 8; ++b) {
-      const uint64_t bal = __ballot((d >> b) & 1u);
-      same &= ((d >> b) & 1u) ? bal : ~bal;
-    }
+    const uint64_t same = __ballot(valid) & ~wave::digit_differs<8>(d);
     const uint32_t r = __popcll(same & lanemask_lt);
     if (valid && r == 0) s_cnt[it][wid][d] = (uint16_t)__popcll(same);
     dig[it] = valid ? d : 256u;

@@ -314,12 +314,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
 #pragma unroll
       for (int it = 0; it < IPT; ++it) {
         const uint32_t d = (uint32_t)(key[it] >> shift) & (RADIX - 1);
-        uint64_t same = ~0ull;
-#pragma unroll
-        for (int b = 0; b < RADIX_BITS; ++b) {
-          const uint64_t bal = __ballot((d >> b) & 1u);
-          same &= ((d >> b) & 1u) ? bal : ~bal;
-        }
+        const uint64_t same = ~wave::digit_differs<RADIX_BITS>(d);
         const uint32_t r = __popcll(same & lanemask_lt);
         if (r == 0) s_cnt[cidx((d * IPT + it) * NW + wid)] = __popcll(same);
         digit[it] = d;

@@ -64,5 +64,21 @@ __device__ inline T all_or(T v) { return lane63(incl(v, Or())); }
 template <typename T>
 __device__ inline T all_and(T v) { return ~all_or<T>(~v); }
 
+// The lanes whose low BITS-bit digit differs from this lane's: one ballot per
+// bit, each lane's bit sign-extended to a whole mask serving both as the
+// ballot's input and as the XOR that turns the ballot into "bit differs".
+template <int BITS>
+__device__ inline uint64_t digit_differs(uint32_t d) {
+  uint32_t lo = 0, hi = 0;  // the mask's halves: lanes 0-31 and 32-63
+#pragma unroll
+  for (int b = 0; b < BITS; ++b) {
+    const uint32_t m = (uint32_t)((int32_t)(d << (31 - b)) >> 31);  // all ones where this lane's bit b is set
+    const uint64_t bal = __ballot(m != 0);
+    lo |= (uint32_t)bal ^ m;
+    hi |= (uint32_t)(bal >> 32) ^ m;
+  }
+  return ((uint64_t)hi << 32) | lo;
+}
+
 }  // namespace wave
 }  // namespace mori
