@@ -9,7 +9,10 @@
 // program's pages.  Each workgroup copies whole units with 16-byte
 // non-temporal loads and stores (every byte is touched once, so nothing is
 // worth caching); the index arithmetic is wavefront-uniform.  A persistent grid
-// walks the units with a grid stride.
+// walks the units with a grid stride.  Runs shorter than a workgroup's pass
+// (1024 threads x two vectors = 32 KiB) are copied several at a time: the
+// workgroup splits into wave-aligned groups of threads, one run each, so every
+// thread still has two vectors in flight.
 //
 //   swap_out : pool page  -> host buffer (direct) or staging (copy engine)
 //   swap_in  : host buffer (direct) or staging -> newly allocated pool page
@@ -50,18 +53,21 @@ __device__ inline uint32_t find_slice(const uint32_t* base, uint32_t n, uint64_t
   return lo;
 }
 
-// Copies n16 vectors with the workgroup's threads; t is the thread index.
-__device__ inline void copy_run(const v4u* __restrict__ src, v4u* __restrict__ dst, uint32_t n16, uint32_t t) {
-  for (uint32_t t0 = 0; t0 < n16; t0 += NT * UNR) {
+constexpr uint32_t MAX_RUNS_PER_PASS = NT / 64;  // groups stay whole wavefronts
+
+// Copies n16 vectors with a group of g threads; t is the thread's index in it.
+__device__ inline void copy_run(const v4u* __restrict__ src, v4u* __restrict__ dst, uint32_t n16, uint32_t g,
+                                uint32_t t) {
+  for (uint32_t t0 = 0; t0 < n16; t0 += g * UNR) {
     v4u v[UNR];
 #pragma unroll
     for (int k = 0; k < UNR; ++k) {
-      const uint32_t i = t0 + k * NT + t;
+      const uint32_t i = t0 + k * g + t;
       if (i < n16) v[k] = __builtin_nontemporal_load(src + i);
     }
 #pragma unroll
     for (int k = 0; k < UNR; ++k) {
-      const uint32_t i = t0 + k * NT + t;
+      const uint32_t i = t0 + k * g + t;
       if (i < n16) __builtin_nontemporal_store(v[k], dst + i);
     }
   }
@@ -142,9 +148,14 @@ __global__ __launch_bounds__(NT) void swap_kernel(SwapArgs s) {
   const uint32_t n = kOut ? s.sum->n_out : s.sum->n_in;
   uint64_t lo, hi;
   if (n == 0 || !unit_range<kOut>(s, n, &lo, &hi)) return;
-  uint64_t u = lo + blockIdx.x;
-  if (u >= hi) return;
   const uint32_t n16 = (uint32_t)(s.run / 16);
+  // runs per pass: the most (a power of two) whose vectors fit two per thread
+  uint32_t per = 1;
+  while (per < MAX_RUNS_PER_PASS && 2ull * per * n16 <= (uint64_t)(NT * UNR)) per *= 2;
+  const uint32_t g = NT / per, grp = threadIdx.x / g, t = threadIdx.x % g;  // g is a multiple of 64
+  const uint64_t stride = (uint64_t)gridDim.x * per;
+  uint64_t u = lo + (uint64_t)blockIdx.x * per + grp;
+  if (u >= hi) return;  // the group's whole wavefronts leave together
   const uint64_t nf = s.sum->pages_free_before + s.sum->pages_dropped;
   Cursor c;
   cursor_set(s, c, find_slice(s.pg_base, n, u / s.LC));
@@ -153,12 +164,12 @@ __global__ __launch_bounds__(NT) void swap_kernel(SwapArgs s) {
   bool ok = unit_ends<kOut>(s, c, u, lo, nf, &src, &dst);
   for (;;) {
     // decode the next unit first: its loads overlap this unit's copy
-    const uint64_t un = u + gridDim.x;
+    const uint64_t un = u + stride;
     const v4u* nsrc = nullptr;
     v4u* ndst = nullptr;
     const bool more = un < hi;
     const bool nok = more && unit_ends<kOut>(s, c, un, lo, nf, &nsrc, &ndst);
-    if (ok) copy_run(src, dst, n16, threadIdx.x);
+    if (ok) copy_run(src, dst, n16, g, t);
     if (!more) break;
     u = un;
     src = nsrc;

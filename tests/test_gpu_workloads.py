@@ -1,7 +1,9 @@
 """The named workloads on the GPU, in the launch configuration bench.py times
 (copy-engine swaps, 2 GiB of staging per direction in two halves, one pinned CPU-tier arena).
 
-Full-size Llama-3-8B, Llama-3-70B and MLA pools (136-155 GiB of HBM): three
+Full-size Llama-3-8B, Llama-3-70B and MLA pools (136-155 GiB of HBM) and one
+rank's share of the Llama-3-70B programs under tensor parallelism of 2 (the
+same programs with 1 KiB rows and 16 KiB runs, 76 GiB): three
 boundary-policy steps, one incremental-policy step and one three-tier (SSD)
 step.  The oracle replays every step's placement and the per-step summaries,
 final block tables, tiers and free map must match exactly; every resident
@@ -20,8 +22,8 @@ from gpu_helpers import log
 from oracle import oracle
 from paper_2606_00866_amd import mori as M
 from paper_2606_00866_amd.tiering import TierPool
-from workload import (CHURN, LLAMA3_70B, LLAMA3_8B, MLA, budget_bytes, churn_steps, fill_pool_torch, make_bank,
-                      make_instance, program_content_torch, run_content, run_tag)
+from workload import (CHURN, LLAMA3_70B, LLAMA3_70B_TP2, LLAMA3_8B, MLA, budget_bytes, churn_steps, fill_pool_torch,
+                      make_bank, make_instance, program_content_torch, run_content, run_tag)
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 GIB = 1 << 30
@@ -135,7 +137,7 @@ class Harness:
         return n_checked
 
 
-@pytest.mark.parametrize("cfg", [LLAMA3_8B, LLAMA3_70B, MLA], ids=lambda c: c.name)
+@pytest.mark.parametrize("cfg", [LLAMA3_8B, LLAMA3_70B, LLAMA3_70B_TP2, MLA], ids=lambda c: c.name)
 def test_full_size_workload(cfg):
     inst = make_instance(cfg)
     total = inst.total_bytes
