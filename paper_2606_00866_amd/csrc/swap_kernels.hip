@@ -55,19 +55,19 @@ __device__ inline uint32_t find_slice(const uint32_t* base, uint32_t n, uint64_t
 
 constexpr uint32_t MAX_RUNS_PER_PASS = NT / 64;  // groups stay whole wavefronts
 
-// Copies n16 vectors with a group of g threads; t is the thread's index in it.
-__device__ inline void copy_run(const v4u* __restrict__ src, v4u* __restrict__ dst, uint32_t n16, uint32_t g,
-                                uint32_t t) {
-  for (uint32_t t0 = 0; t0 < n16; t0 += g * UNR) {
+// Copies n16 vectors with a group of G threads; t is the thread's index in it.
+template <uint32_t G>
+__device__ inline void copy_run(const v4u* __restrict__ src, v4u* __restrict__ dst, uint32_t n16, uint32_t t) {
+  for (uint32_t t0 = 0; t0 < n16; t0 += G * UNR) {
     v4u v[UNR];
 #pragma unroll
     for (int k = 0; k < UNR; ++k) {
-      const uint32_t i = t0 + k * g + t;
+      const uint32_t i = t0 + k * G + t;
       if (i < n16) v[k] = __builtin_nontemporal_load(src + i);
     }
 #pragma unroll
     for (int k = 0; k < UNR; ++k) {
-      const uint32_t i = t0 + k * g + t;
+      const uint32_t i = t0 + k * G + t;
       if (i < n16) __builtin_nontemporal_store(v[k], dst + i);
     }
   }
@@ -142,19 +142,18 @@ __device__ inline bool unit_ends(const SwapArgs& s, Cursor& c, uint64_t u, uint6
   return true;
 }
 
-template <bool kOut>
+// PER runs per pass (runs_per_pass below, chosen on the host from the run size)
+template <bool kOut, uint32_t PER>
 __global__ __launch_bounds__(NT) void swap_kernel(SwapArgs s) {
   if (s.sum->error || *s.swap_err) return;
   const uint32_t n = kOut ? s.sum->n_out : s.sum->n_in;
   uint64_t lo, hi;
   if (n == 0 || !unit_range<kOut>(s, n, &lo, &hi)) return;
   const uint32_t n16 = (uint32_t)(s.run / 16);
-  // runs per pass: the most (a power of two) whose vectors fit two per thread
-  uint32_t per = 1;
-  while (per < MAX_RUNS_PER_PASS && 2ull * per * n16 <= (uint64_t)(NT * UNR)) per *= 2;
-  const uint32_t g = NT / per, grp = threadIdx.x / g, t = threadIdx.x % g;  // g is a multiple of 64
-  const uint64_t stride = (uint64_t)gridDim.x * per;
-  uint64_t u = lo + (uint64_t)blockIdx.x * per + grp;
+  constexpr uint32_t G = NT / PER;  // threads per run, whole wavefronts
+  const uint32_t grp = threadIdx.x / G, t = threadIdx.x % G;
+  const uint64_t stride = (uint64_t)gridDim.x * PER;
+  uint64_t u = lo + (uint64_t)blockIdx.x * PER + grp;
   if (u >= hi) return;  // the group's whole wavefronts leave together
   const uint64_t nf = s.sum->pages_free_before + s.sum->pages_dropped;
   Cursor c;
@@ -169,7 +168,7 @@ __global__ __launch_bounds__(NT) void swap_kernel(SwapArgs s) {
     v4u* ndst = nullptr;
     const bool more = un < hi;
     const bool nok = more && unit_ends<kOut>(s, c, un, lo, nf, &nsrc, &ndst);
-    if (ok) copy_run(src, dst, n16, g, t);
+    if (ok) copy_run<G>(src, dst, n16, t);
     if (!more) break;
     u = un;
     src = nsrc;
@@ -178,16 +177,31 @@ __global__ __launch_bounds__(NT) void swap_kernel(SwapArgs s) {
   }
 }
 
+// Runs per pass: the most (a power of two, at most one per wavefront) whose
+// vectors still fill two per thread of the workgroup.
+uint32_t runs_per_pass(uint64_t run) {
+  const uint64_t n16 = run / 16;
+  uint32_t per = 1;
+  while (per < MAX_RUNS_PER_PASS && 2ull * per * n16 <= (uint64_t)(NT * UNR)) per *= 2;
+  return per;
+}
+
+template <bool kOut>
+hipError_t launch_swap(const SwapArgs& a, uint32_t grid, hipStream_t s) {
+  switch (runs_per_pass(a.run)) {
+    case 1: hipLaunchKernelGGL((swap_kernel<kOut, 1>), dim3(grid), dim3(NT), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((swap_kernel<kOut, 2>), dim3(grid), dim3(NT), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((swap_kernel<kOut, 4>), dim3(grid), dim3(NT), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((swap_kernel<kOut, 8>), dim3(grid), dim3(NT), 0, s, a); break;
+    default: hipLaunchKernelGGL((swap_kernel<kOut, 16>), dim3(grid), dim3(NT), 0, s, a); break;
+  }
+  return hipGetLastError();
+}
+
 }  // namespace
 
-hipError_t launch_swap_out(const SwapArgs& a, uint32_t grid, hipStream_t s) {
-  hipLaunchKernelGGL(swap_kernel<true>, dim3(grid), dim3(NT), 0, s, a);
-  return hipGetLastError();
-}
+hipError_t launch_swap_out(const SwapArgs& a, uint32_t grid, hipStream_t s) { return launch_swap<true>(a, grid, s); }
 
-hipError_t launch_swap_in(const SwapArgs& a, uint32_t grid, hipStream_t s) {
-  hipLaunchKernelGGL(swap_kernel<false>, dim3(grid), dim3(NT), 0, s, a);
-  return hipGetLastError();
-}
+hipError_t launch_swap_in(const SwapArgs& a, uint32_t grid, hipStream_t s) { return launch_swap<false>(a, grid, s); }
 
 }  // namespace mori
