@@ -564,3 +564,26 @@ def test_pools_around_the_tile_scan_switch(target):
         assert recycled > 0
     finally:
         pair.close()
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("row_bytes,tokens", [(2048, 16), (1024, 16), (256, 16), (128, 16), (16, 4)],
+                         ids=["32KiB", "16KiB", "4KiB", "2KiB", "64B"])
+def test_runs_per_pass(row_bytes, tokens, mode):
+    """Runs of 32 KiB (one per workgroup pass), 16, 4 and 2 KiB (two, four and
+    eight per pass) and 64 B (sixteen): every byte lands where the oracle puts
+    it, three steps with swaps both ways."""
+    rng = np.random.default_rng(row_bytes * 100 + tokens)
+    geom = Geometry(layers=2, planes=2, block_tokens=tokens, row_bytes=row_bytes, num_blocks=0)
+    inst = random_instance(rng, P=40, max_blocks=12, geom=geom, tier_p=(0.5, 0.3, 0.2), extra_free=20)
+    log(f"runs per pass: run={row_bytes * tokens} B mode={mode} NB={inst.geom.num_blocks}")
+    pair = Pair(inst, seed=row_bytes + tokens, staging_bytes=int(rng.choice([0, 5 * inst.geom.run_bytes])))
+    try:
+        bb = inst.geom.block_bytes
+        for step in range(3):
+            w = inst.window if step % 2 == 0 else inst.window[:, :, ::-1].copy()
+            res, plan = pair.step(gpu_bytes=inst.geom.num_blocks * bb * 2 // 3 // bb * bb,
+                                  cpu_bytes=inst.total_bytes // 3 // bb * bb, window=w, mode=mode)
+            assert res.rc == oracle.OK and plan is not None
+    finally:
+        pair.close()
