@@ -39,8 +39,10 @@
 //     - scatter: the same ranking and position, with the lower tiles' count
 //       read from the scanned histogram;
 //   prefix   inclusive u64 scan of block bytes in eviction order (tile scans,
-//            one-workgroup scan of tile totals, fix-up) and the number of
-//            evictions that frees the requested bytes.
+//            then a fix-up whose workgroups each sum the tile totals below
+//            their tile, or above FIX_SCAN_TILES a one-workgroup scan of the
+//            tile totals first) and the number of evictions that frees the
+//            requested bytes.
 //
 // Everything is latency-bound at 10^5-10^6 blocks (tens of microseconds);
 // the workspace is the caller's, so nothing is allocated here.
@@ -65,6 +67,10 @@ constexpr uint32_t TOT_SPLIT = 8;        // totals: workgroups per pass, each su
 // kernels (histogram, per-digit scan, scatter): each look-back round is a
 // device-coherent load, so the look-back chains grow with the tile count.
 constexpr uint32_t ONESWEEP_TILES = 128;
+// Tile counts up to this finish the prefix with one kernel (every workgroup
+// reads the tile totals: 8 B each) instead of a tile scan, a fix-up and a
+// result kernel.
+constexpr uint32_t FIX_SCAN_TILES = 1024;
 constexpr uint64_t ST_AGG = 1ull << 32;  // status flags: the tile's own count ...
 constexpr uint64_t ST_INCL = 2ull << 32; // ... or its inclusive count over tiles 0..t
 constexpr uint32_t SPIN_LIMIT = 1u << 22;  // polls of one status word before reporting a stall
@@ -582,6 +588,71 @@ __global__ __launch_bounds__(ET) void evict_prefix_fix_kernel(EvictArgs a) {
   }
 }
 
+// Up to FIX_SCAN_TILES tiles: the fix-up workgroups scan the tile totals
+// themselves (each sums the totals below its tile) and the result comes from
+// the one workgroup whose tile holds the first prefix >= need (the prefix never
+// decreases, so that tile is unique; without one, the last tile's workgroup
+// reports every block), so neither the one-workgroup tile scan nor the result
+// kernel runs.
+template <int EIPT>
+__global__ __launch_bounds__(ET) void evict_prefix_fix_scan_kernel(EvictArgs a) {
+  __shared__ uint64_t s_red[ENW][2];
+  if (a.misc[2]) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      a.result[0] = 0;
+      a.result[1] = (uint32_t)a.misc[2];
+    }
+    return;
+  }
+  uint64_t below = 0, all = 0;  // totals of the tiles below this one, and of every tile
+  for (uint32_t t = threadIdx.x; t < a.ntiles; t += ET) {
+    const uint64_t v = a.tile_sum[t];
+    if (t < blockIdx.x) below += v;
+    all += v;
+  }
+  below = wave::sum(below);
+  all = wave::sum(all);
+  if ((threadIdx.x & 63) == 0) {
+    s_red[threadIdx.x >> 6][0] = below;
+    s_red[threadIdx.x >> 6][1] = all;
+  }
+  __syncthreads();
+  below = all = 0;
+#pragma unroll
+  for (int w = 0; w < ENW; ++w) {
+    below += s_red[w][0];
+    all += s_red[w][1];
+  }
+  const uint64_t base = (uint64_t)blockIdx.x * (ET * EIPT);
+  uint32_t short_of_need = 0;
+  for (int it = 0; it < EIPT; ++it) {
+    const uint64_t i = base + it * ET + threadIdx.x;
+    if (i < a.N) {
+      const uint64_t p = a.prefix[i] + below;
+      a.prefix[i] = p;
+      short_of_need += p < a.need;
+    }
+  }
+  __syncthreads();  // s_red is reused
+  short_of_need = wave::sum(short_of_need);
+  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6][0] = short_of_need;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t c = 0;
+    for (int w = 0; w < ENW; ++w) c += s_red[w][0];
+    const uint64_t len = a.N - base < (uint64_t)(ET * EIPT) ? a.N - base : (uint64_t)(ET * EIPT);
+    const bool last = blockIdx.x == a.ntiles - 1;
+    if (blockIdx.x == 0) a.result[1] = 0;
+    if (a.need == 0) {
+      if (blockIdx.x == 0) a.result[0] = 0;
+    } else if (below < a.need && c < len) {  // the first prefix >= need is in this tile
+      a.result[0] = (uint32_t)(base + c + 1);
+    } else if (last && all < a.need) {  // no prefix reaches need: every block
+      a.result[0] = a.N;
+    }
+  }
+}
+
 __global__ void evict_result_kernel(EvictArgs a) {
   const uint64_t err = a.misc[2];
   uint64_t count = 0;
@@ -605,8 +676,13 @@ void launch_tiles(const EvictArgs& a, hipStream_t s) {
     }
   }
   hipLaunchKernelGGL(evict_prefix_tiles_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a);
-  hipLaunchKernelGGL(evict_prefix_top_kernel, dim3(1), dim3(1024), 0, s, a);
-  hipLaunchKernelGGL(evict_prefix_fix_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a);
+  if (a.ntiles <= FIX_SCAN_TILES) {
+    hipLaunchKernelGGL(evict_prefix_fix_scan_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a);
+  } else {
+    hipLaunchKernelGGL(evict_prefix_top_kernel, dim3(1), dim3(1024), 0, s, a);
+    hipLaunchKernelGGL(evict_prefix_fix_kernel<EIPT>, dim3(a.ntiles), dim3(ET), 0, s, a);
+    hipLaunchKernelGGL(evict_result_kernel, dim3(1), dim3(1), 0, s, a);
+  }
 }
 
 }  // namespace
@@ -674,8 +750,9 @@ hipError_t launch_evict(uint32_t N, const uint8_t* type, const uint64_t* last_ac
   if (a.ntiles) {
     if (kpt == 4) launch_tiles<4>(a, s);
     else launch_tiles<8>(a, s);
+  } else {
+    hipLaunchKernelGGL(evict_result_kernel, dim3(1), dim3(1), 0, s, a);
   }
-  hipLaunchKernelGGL(evict_result_kernel, dim3(1), dim3(1), 0, s, a);
   return hipGetLastError();
 }
 

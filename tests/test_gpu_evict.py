@@ -155,3 +155,30 @@ def test_python_wrapper():
     assert np.array_equal(order.cpu().numpy().view(np.uint32), o_order)
     assert np.array_equal(prefix.cpu().numpy().view(np.uint64), o_prefix)
     assert result.cpu().tolist() == [o_count, 0]
+
+
+def test_need_at_prefix_edges():
+    """The eviction count when need is 0, equals a prefix value exactly (at the
+    first block, at tile edges, at the last block), lies just above one, or
+    exceeds every block's bytes: each equals the oracle's."""
+    rng = np.random.default_rng(5)
+    N = 5000  # five tiles of 1024 keys
+    typ, la, size = eviction_blocks(rng, N, programs=40, tie_frac=0.5, var_size=True)
+    rc, _, prefix, _ = oracle.evict_order(typ, la, 0, 0, size=size, unit_bytes=1)
+    assert rc == oracle.OK
+    p = [int(x) for x in prefix]
+    for need in (0, 1, p[0], p[0] + 1, p[1022], p[1023], p[1023] + 1, p[1024], p[2047], p[4095], p[-2], p[-1],
+                 p[-1] + 1, 10 * p[-1]):
+        log(f"evict need={need}")
+        check(typ, la, size, 1, 0, need)
+
+
+def test_more_tiles_than_the_single_kernel_tail():
+    """2^21 + 5000 blocks: 1027 tiles of 2048 keys, so the prefix is finished by
+    the tile-total scan, the fix-up and the result kernel."""
+    N = (1 << 21) + 5000
+    rng = np.random.default_rng(N)
+    typ, la, size = eviction_blocks(rng, N, programs=4096, tie_frac=0.5, var_size=True)
+    total = int(size.astype(np.int64).sum())
+    log(f"evict N={N}")
+    check(typ, la, size, 4096, 1, total * 4096 // 2)
