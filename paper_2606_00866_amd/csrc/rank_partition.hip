@@ -106,7 +106,7 @@ __device__ inline uint8_t category(uint8_t from, uint8_t to) {
 template <int RT, int IPT>
 __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
   constexpr int NW = RT / 64;  // wavefronts
-  constexpr int NCNT = RADIX * IPT * NW;  // digit counters, (digit, item slice, wave)
+  constexpr int NCNT = RADIX * NW;  // digit counters, (digit, wave)
   constexpr int CPT = NCNT / RT;         // consecutive counters per thread in their scan
   static_assert(NCNT % RT == 0, "whole counters per thread");
   // counter c lives at c + c / 32: a thread's CPT consecutive counters then
@@ -300,15 +300,37 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     __syncthreads();
   } else {
     // LSD radix sort, 8-bit digits (at most four passes over idleness keys).
-    // Digit counters are laid out (digit, it, wave) so an exclusive scan over
-    // them in index order gives every (digit, item slice, wave) its output
-    // base in (digit, original position) order, i.e. a stable pass.  Digits
-    // on which every real key agrees are skipped; padding keeps the tail.
-    // Five barriers a pass: counts, wave totals, bases, scatter, and the
+    // During the sort each wave holds a block of 64 * IPT consecutive
+    // positions (slice it of wave w: positions w * 64 * IPT + it * 64 + lane)
+    // and ranks its slices in order, a running count per (digit, wave) in LDS
+    // carrying the ranks from slice to slice; those counters, scanned in
+    // (digit, wave) order, give every group its output base, so a pass is
+    // stable.  Items move to the blocked order before the first pass and back
+    // to the striped one (item it of thread tid at it * RT + tid) in the last.
+    // Digits on which every real key agrees are skipped; padding keeps the
+    // tail.  Five barriers a pass: counts, wave totals, bases, scatter, and the
     // read-back that also clears the next pass's counters.
     const uint64_t varying = s_or ^ s_and;
     const uint64_t lanemask_lt = (1ull << lane) - 1ull;
-    for (int shift = 0; shift < KEY_BITS; shift += RADIX_BITS) {
+    int last_shift = -1;
+    for (int shift = 0; shift < KEY_BITS; shift += RADIX_BITS)
+      if ((varying >> shift) & (RADIX - 1)) last_shift = shift;
+    const uint32_t blk = (uint32_t)wid * 64 * IPT + lane;  // this lane's position in slice 0
+    if (IPT > 1 && last_shift >= 0) {  // to the blocked order (positions are program ids here)
+#pragma unroll
+      for (int it = 0; it < IPT; ++it) {
+        s_key[it * RT + tid] = key[it];
+        s_id[it * RT + tid] = id[it];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int it = 0; it < IPT; ++it) {
+        key[it] = s_key[blk + it * 64];
+        id[it] = s_id[blk + it * 64];
+      }
+      // the first pass overwrites s_key only after its first barriers
+    }
+    for (int shift = 0; shift <= last_shift; shift += RADIX_BITS) {
       if (((varying >> shift) & (RADIX - 1)) == 0) continue;
       uint32_t digit[IPT], lrank[IPT];
 #pragma unroll
@@ -316,9 +338,13 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
         const uint32_t d = (uint32_t)(key[it] >> shift) & (RADIX - 1);
         const uint64_t same = ~wave::digit_differs<RADIX_BITS>(d);
         const uint32_t r = __popcll(same & lanemask_lt);
-        if (r == 0) s_cnt[cidx((d * IPT + it) * NW + wid)] = __popcll(same);
+        const uint32_t c = cidx(d * NW + wid);
+        const uint32_t before = s_cnt[c];  // keys of digit d in this wave's earlier slices
+        __builtin_amdgcn_wave_barrier();
+        if (r == 0) s_cnt[c] = before + __popcll(same);  // read by the next slice's lanes
+        __builtin_amdgcn_wave_barrier();
         digit[it] = d;
-        lrank[it] = r;
+        lrank[it] = before + r;
       }
       __syncthreads();
       uint32_t loc[CPT], sum = 0;
@@ -341,15 +367,16 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
       __syncthreads();
 #pragma unroll
       for (int it = 0; it < IPT; ++it) {
-        const uint32_t pos = s_cnt[cidx((digit[it] * IPT + it) * NW + wid)] + lrank[it];
+        const uint32_t pos = s_cnt[cidx(digit[it] * NW + wid)] + lrank[it];
         s_key[pos] = key[it];
         s_id[pos] = id[it];
       }
       __syncthreads();
 #pragma unroll
       for (int it = 0; it < IPT; ++it) {
-        key[it] = s_key[it * RT + tid];
-        id[it] = s_id[it * RT + tid];
+        const uint32_t x = shift == last_shift ? it * RT + tid : blk + it * 64;  // striped after the last pass
+        key[it] = s_key[x];
+        id[it] = s_id[x];
       }
 #pragma unroll
       for (int j = 0; j < CPT; ++j) s_cnt[cidx(j * RT + tid)] = 0;  // every base of this pass is read
