@@ -266,6 +266,42 @@ __device__ inline uint32_t scan256(uint32_t v, uint32_t* s_w, uint32_t* total) {
   return before + x - v;
 }
 
+// The tile's keys to their global positions, staged through LDS in the
+// tile's digit order so that each wave's stores cover a few contiguous runs
+// (one per digit it meets) instead of one scattered 8-byte store per lane.
+// s_tstart[d]: first tile-local slot of digit d; s_off[d]: its global slot;
+// s_cnt: the (slice, wave, digit) offsets within each digit; n: valid keys.
+// Every thread calls it; it begins and ends with a barrier.
+template <int EIPT>
+__device__ void store_tile(const uint64_t (&key)[EIPT], const uint32_t (&val)[EIPT], const uint32_t (&dig)[EIPT],
+                           const uint32_t (&rnk)[EIPT], const uint16_t (*s_cnt)[ENW][256], const uint32_t* s_tstart,
+                           const uint32_t* s_off, uint64_t* s_k, uint32_t* s_v, uint32_t n, int shift, uint64_t* kd,
+                           uint32_t* vd) {
+  const int tid = threadIdx.x, wid = tid >> 6;
+  __syncthreads();
+#pragma unroll
+  for (int it = 0; it < EIPT; ++it) {
+    const uint32_t d = dig[it];
+    if (d < 256u) {
+      const uint32_t local = s_tstart[d] + s_cnt[it][wid][d] + rnk[it];
+      s_k[local] = key[it];
+      s_v[local] = val[it];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < EIPT; ++j) {
+    const uint32_t local = j * ET + tid;
+    if (local < n) {
+      const uint64_t k = s_k[local];
+      const uint32_t d = (uint32_t)(k >> shift) & 255u;
+      const uint32_t pos = s_off[d] + (local - s_tstart[d]);
+      kd[pos] = k;
+      vd[pos] = s_v[local];
+    }
+  }
+}
+
 // One workgroup per digit: exclusive scan of hist[digit][0..ntiles) in place
 // and the digit's total.
 __global__ __launch_bounds__(ET) void evict_dscan_kernel(EvictArgs a, int shift) {
@@ -289,7 +325,10 @@ __global__ __launch_bounds__(ET) void evict_scatter_kernel(EvictArgs a, int shif
   // s_cnt[slice][wave][digit]: keys of that digit in that wave's 64 keys of the
   // slice, then (after the per-digit scan) their offset within the tile
   __shared__ uint16_t s_cnt[EIPT][ENW][256];
-  __shared__ uint32_t s_off[256];  // this tile's global base per digit
+  __shared__ uint32_t s_off[256];     // this tile's global base per digit
+  __shared__ uint32_t s_tstart[256];  // ... and its first slot within the tile
+  __shared__ uint64_t s_k[ET * EIPT];
+  __shared__ uint32_t s_v[ET * EIPT];
   __shared__ uint32_t s_w[ENW];
   if (a.misc[2] || !digit_varies(a, shift)) return;
   const int src = source_buffer(a, shift);
@@ -327,27 +366,18 @@ __global__ __launch_bounds__(ET) void evict_scatter_kernel(EvictArgs a, int shif
     rnk[it] = r;
   }
   __syncthreads();
-  {  // per digit (one per thread): offsets in (slice, wave) order, i.e. original key order
-    uint32_t run = 0;
+  uint32_t run = 0;  // per digit (one per thread): offsets in (slice, wave) order, i.e. original key order
 #pragma unroll
-    for (int it = 0; it < EIPT; ++it)
+  for (int it = 0; it < EIPT; ++it)
 #pragma unroll
-      for (int w = 0; w < ENW; ++w) {
-        const uint32_t c = s_cnt[it][w][tid];
-        s_cnt[it][w][tid] = (uint16_t)run;
-        run += c;
-      }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int it = 0; it < EIPT; ++it) {
-    const uint32_t d = dig[it];
-    if (d < 256u) {
-      const uint32_t pos = s_off[d] + s_cnt[it][wid][d] + rnk[it];
-      kd[pos] = key[it];
-      vd[pos] = val[it];
+    for (int w = 0; w < ENW; ++w) {
+      const uint32_t c = s_cnt[it][w][tid];
+      s_cnt[it][w][tid] = (uint16_t)run;
+      run += c;
     }
-  }
+  uint32_t n;
+  s_tstart[tid] = scan256(run, s_w, &n);
+  store_tile<EIPT>(key, val, dig, rnk, s_cnt, s_tstart, s_off, s_k, s_v, n, shift, kd, vd);
 }
 
 // Keys per digit of every pass: workgroup (pass, share) sums a share of the
@@ -467,6 +497,8 @@ __global__ __launch_bounds__(ET) void evict_pass_kernel(EvictArgs a, int shift) 
     }
     status_store(mine, ST_INCL | (uint64_t)(before + run));
   }
+  // stores straight from registers: at up to 128 tiles, staging them through
+  // LDS in digit order (as the three-kernel scatter does) measured slower
   uint32_t tot;
   const uint32_t digit_base = scan256(total_d, s_w, &tot);
   s_off[tid] = digit_base + before;
