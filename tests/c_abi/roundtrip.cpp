@@ -4,7 +4,11 @@
 // budget with skip-fit), alternating the copy modes, each compared with the
 // CPU oracle bit for bit: the plan (order, prefix, categories, summary), the
 // block tables, tiers and free map, every byte of the resident pages and of
-// the CPU tier's host buffers.
+// the CPU tier's host buffers.  The swaps' kernel timing records (each
+// direction's payload equals the plans' bytes), the typed eviction order of
+// random KV blocks on both tiers (Sec. 4.3.2) and the multi-replica admission
+// of a random Waiting queue with both rules (Sec. 4.1, Sec. 4.3.1), each
+// against the same oracle.
 //
 //   roundtrip <programs> <seed>      exit status 0 when everything matches
 #include <hip/hip_runtime.h>
@@ -162,6 +166,8 @@ int main(int argc, char** argv) {
   std::vector<uint8_t*> obuf_ptr(P);
   for (uint32_t p = 0; p < P; ++p) obuf_ptr[p] = obuf[p].data();
 
+  MORI_OK_(mori_profile(ctx, 1));
+  uint64_t moved[2] = {0, 0};  // plans' bytes per direction
   for (int step = 0; step < 3; ++step) {
     if (step == 1)  // the reversed ranking: each program's reasoning and tool time swap
       for (size_t i = 0; i < window.size(); i += 2) std::swap(window[i], window[i + 1]);
@@ -198,6 +204,8 @@ int main(int argc, char** argv) {
       EXPECT(plan.order[r] == o_order[r] && plan.prefix[r] == o_prefix[r], "step %d rank %u", step, r);
       EXPECT(plan.category[r] == o_cat[r] && plan.tier_old[r] == o_told[r], "step %d program %u", step, r);
     }
+    moved[0] += plan.bytes_out;
+    moved[1] += plan.bytes_in;
     // the caller's part: nothing to place, every program keeps its extent
     MORI_OK_(mori_kv_swap_out(ctx, host_addr.data(), mode, s_out));
     MORI_OK_(mori_kv_swap_in(ctx, host_addr.data(), mode, s_in));
@@ -237,7 +245,100 @@ int main(int argc, char** argv) {
                 (unsigned long long)pages, cpu_programs);
   }
 
+  for (int d = 0; d < 2; ++d) {  // kernel timing: one record per swap launch
+    uint64_t launches = 0, payload = 0;
+    double ms = -1.0;
+    MORI_OK_(mori_profile_read(ctx, d, &launches, &payload, &ms));
+    EXPECT(payload == moved[d], "direction %d profiled payload %llu of %llu", d, (unsigned long long)payload,
+           (unsigned long long)moved[d]);
+    EXPECT((launches > 0) == (moved[d] > 0) && ms >= 0.0, "direction %d launches %llu", d,
+           (unsigned long long)launches);
+    MORI_OK_(mori_profile_read(ctx, d, &launches, &payload, &ms));  // a read clears the record
+    EXPECT(launches == 0 && payload == 0, "direction %d record not cleared", d);
+  }
+  std::printf("profiling: %llu B out, %llu B in recorded\n", (unsigned long long)moved[0],
+              (unsigned long long)moved[1]);
   MORI_OK_(mori_destroy(ctx));
+
+  // ---- typed eviction order of random KV blocks, both tiers ----------------
+  {
+    const uint32_t N = 3000 + rng.below(5000);
+    std::vector<uint8_t> type(N);
+    std::vector<uint64_t> last(N);
+    std::vector<uint32_t> size(N);
+    uint64_t total = 0;
+    for (uint32_t i = 0; i < N; ++i) {  // runs of blocks sharing a program's label and, often, its time
+      const bool fresh = i == 0 || rng.below(8) == 0;
+      type[i] = fresh ? (uint8_t)rng.below(3) : type[i - 1];
+      last[i] = fresh || rng.below(2) ? rng.next() >> 24 : last[i - 1];
+      size[i] = 1 + rng.below(16);
+      total += size[i];
+    }
+    const uint8_t* d_type = dev_copy(type);
+    const uint64_t* d_last = dev_copy(last);
+    const uint32_t* d_size = dev_copy(size);
+    uint64_t ws_bytes = 0;
+    MORI_OK_(mori_evict_workspace(N, &ws_bytes));
+    void* ws = nullptr;
+    uint32_t *d_order = nullptr, *d_result = nullptr;
+    uint64_t* d_prefix = nullptr;
+    HIP_OK(hipMalloc(&ws, ws_bytes));
+    HIP_OK(hipMalloc(&d_order, 4ull * N));
+    HIP_OK(hipMalloc(&d_prefix, 8ull * N));
+    HIP_OK(hipMalloc(&d_result, 8));
+    const mori_blocks blocks{N, d_type, d_last, d_size, 4096};
+    for (uint32_t tier_e : {MORI_TIER_GPU, MORI_TIER_CPU}) {
+      const uint64_t need = (uint64_t)rng.below((uint32_t)total + 1) * 4096;
+      MORI_OK_(mori_evict_order(&blocks, tier_e, need, ws, ws_bytes, d_order, d_prefix, d_result, s_out));
+      HIP_OK(hipStreamSynchronize(s_out));
+      std::vector<uint32_t> o_ord(N);
+      std::vector<uint64_t> o_pre(N);
+      uint32_t o_count = 0;
+      EXPECT(orc_evict_order(N, type.data(), last.data(), size.data(), 4096, tier_e, need, o_ord.data(),
+                             o_pre.data(), &o_count) == ORC_OK,
+             "oracle eviction order");
+      const auto g_ord = host_copy(d_order, N);
+      const auto g_pre = host_copy(d_prefix, N);
+      const auto g_res = host_copy(d_result, 2);
+      EXPECT(g_ord == o_ord && g_pre == o_pre, "eviction order tier %u", tier_e);
+      EXPECT(g_res[0] == o_count && g_res[1] == 0, "eviction count tier %u: %u vs %u", tier_e, g_res[0], o_count);
+      std::printf("eviction order: %u blocks, tier %u, %u evictions free %llu B\n", N, tier_e, g_res[0],
+                  (unsigned long long)need);
+    }
+    for (void* d : {ws, (void*)d_order, (void*)d_prefix, (void*)d_result, (void*)d_type, (void*)d_last,
+                    (void*)d_size})
+      HIP_OK(hipFree(d));
+  }
+
+  // ---- multi-replica admission of a Waiting queue (host memory) -----------
+  {
+    const uint32_t W = 300, R = 8;
+    std::vector<uint64_t> bytes(W), room(R);
+    std::vector<float> iota(W);
+    std::vector<uint8_t> st(W);
+    uint64_t want = 0;
+    for (uint32_t p = 0; p < W; ++p) {
+      bytes[p] = (uint64_t)(1 + rng.below(64)) << 21;
+      iota[p] = (float)rng.below(1001) / 1000.0f;
+      st[p] = (uint8_t)rng.below(3);
+      want += bytes[p];
+    }
+    for (uint32_t r = 0; r < R; ++r) room[r] = (uint64_t)rng.below((uint32_t)(want >> 21) / 4 + 1) << 21;
+    for (uint32_t flags_a : {0u, (uint32_t)MORI_ADMIT_BEST_FIT}) {
+      std::vector<int32_t> rep_g(W), rep_o(W);
+      std::vector<uint64_t> after_g(R), after_o(R);
+      MORI_OK_(mori_replica_admit(W, bytes.data(), iota.data(), st.data(), R, room.data(), flags_a, rep_g.data(),
+                                  after_g.data()));
+      EXPECT(orc_replica_admit(W, bytes.data(), iota.data(), st.data(), R, room.data(), flags_a, rep_o.data(),
+                               after_o.data()) == ORC_OK,
+             "oracle replica admission");
+      EXPECT(rep_g == rep_o && after_g == after_o, "replica admission flags %u", flags_a);
+      uint32_t admitted = 0;
+      for (int32_t r : rep_g) admitted += r >= 0;
+      std::printf("replica admission (%s): %u of %u waiting programs placed on %u replicas\n",
+                  flags_a ? "best fit" : "most room", admitted, W, R);
+    }
+  }
   MORI_OK_(mori_host_free(arena));
   HIP_OK(hipStreamDestroy(s_out));
   HIP_OK(hipStreamDestroy(s_in));

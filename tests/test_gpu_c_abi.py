@@ -1,7 +1,9 @@
 """The C ABI used from C: tests/c_abi/roundtrip drives libmori with plain
-pointers and HIP runtime calls (no Python, no torch) through three rebalances
-and compares every result with the C oracle bit for bit.  Run as a child
-process, one per program count, covering the rank kernel's three shapes."""
+pointers and HIP runtime calls (no Python, no torch) through three rebalances,
+the kernel timing records, a typed eviction order on both tiers and a
+multi-replica admission with both rules, and compares every result with the C
+oracle bit for bit.  Run as a child process, one per program count, covering
+the rank kernel's three shapes."""
 import os
 import subprocess
 
