@@ -22,7 +22,8 @@
 //      swap-out and swap-in lists in that order and the page/slot bases.
 //
 // P <= 4096 programs fit in LDS (4 keys per thread), so the whole step is one
-// launch of a few microseconds; nothing here is bandwidth-bound.
+// launch: microseconds for tens of programs, about thirty for 4096, bound by
+// the one workgroup's vector ALU and barriers; nothing here is bandwidth-bound.
 #include "mori_internal.h"
 #include "wave.h"
 
@@ -32,7 +33,7 @@ namespace {
 // Three shapes, chosen by P at launch: 256 threads x 1 item for P <= 256
 // (barriers over 4 waves; ranks counted directly), 1024 x 1 up to 1024 and
 // 1024 threads x 4 items (striped: item x = it * RT + tid) up to 4096; fewer
-// item slices mean fewer ballots and digit counters per radix pass.
+// item slices mean fewer ballots per radix pass.
 constexpr int RADIX_BITS = 8;
 constexpr int RADIX = 1 << RADIX_BITS;
 constexpr int KEY_BITS = 64;
