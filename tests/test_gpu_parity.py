@@ -8,7 +8,7 @@ import torch
 from gpu_helpers import Pair, log
 from oracle import oracle
 from paper_2606_00866_amd import mori as M
-from paper_2606_00866_amd.tiering import TierPool
+from paper_2606_00866_amd.tiering import MoriError, TierPool
 from workload import TINY, Geometry, budget_bytes, make_instance, random_instance
 
 pytestmark = pytest.mark.gpu
@@ -587,3 +587,49 @@ def test_runs_per_pass(row_bytes, tokens, mode):
             assert res.rc == oracle.OK and plan is not None
     finally:
         pair.close()
+
+
+SUMMARY = ("m_gpu", "m_cpu", "n_out", "n_in", "n_drop_gpu", "n_drop_cpu", "n_admit_gpu", "n_admit_cpu", "pages_out",
+           "pages_in", "pages_admit", "pages_free_before", "pages_released", "pages_recycled", "pages_free_after",
+           "bytes_out", "bytes_in", "gpu_bytes_after", "cpu_bytes_after")
+
+
+def test_plans_supersede_without_swaps():
+    """Placement-only use: four plans in a row with no swap in between (each
+    new plan supersedes the last; tables, tiers and the free map stand as the
+    last plan wrote them), each equal to the oracle's placement from the state
+    the previous one left -- summary, tables, tiers, free map.  Then the last
+    plan's swaps: its swap-ins read host buffers that the skipped swap-outs
+    never filled or placed, so the device refuses them (MORI_DEV_HOST_ADDR)
+    and reports it, rather than copying from an unregistered address."""
+    rng = np.random.default_rng(606)
+    geom = Geometry(layers=2, planes=2, block_tokens=2, row_bytes=64, num_blocks=0)
+    inst = random_instance(rng, P=120, max_blocks=10, geom=geom, tier_p=(0.5, 0.3, 0.2), extra_free=40)
+    tp = TierPool(inst.geom, inst.tbl_off, inst.tbl, inst.tier, inst.free_map, arena_bytes=1 << 20)
+    try:
+        tbl, tier, free = inst.copy_state()
+        bb = inst.geom.block_bytes
+        for step in range(4):
+            w = rng.choice(np.array([0.0, 0.5, 1.0, 2.0, 8.0], np.float32), size=inst.window.shape)
+            bg = int(rng.integers(0, inst.geom.num_blocks + 1)) * bb
+            bc = int(rng.integers(0, inst.total_bytes // bb + 1)) * bb
+            res = oracle.rebalance(inst.geom, window=w, tbl_off=inst.tbl_off, tbl=tbl, tier=tier, free_map=free,
+                                   gpu_budget=bg, cpu_budget=bc)
+            assert res.rc == oracle.OK
+            assert tp.rank_partition(gpu_bytes=bg, cpu_bytes=bc, window=torch.from_numpy(w).cuda()) == M.MORI_OK
+            rc, plan = tp.plan_wait()
+            assert rc == M.MORI_OK
+            for k in SUMMARY:
+                assert getattr(plan, k) == res.summary[k], (step, k)
+            g_tbl, g_tier, g_free = tp.state()
+            assert (g_tbl == tbl).all() and (g_tier == tier).all() and (g_free == free).all(), step
+            log(f"placement-only plan {step}: out {plan.n_out} in {plan.n_in} admitted {plan.n_admit_gpu}")
+        assert plan.n_in > 0
+        tp.place_host_buffers()
+        assert tp.swap_out(M.MORI_COPY_KERNEL) == M.MORI_OK
+        assert tp.swap_in(M.MORI_COPY_KERNEL) == M.MORI_OK
+        with pytest.raises(MoriError) as e:
+            tp.synchronize()
+        assert e.value.code == M.MORI_EDEVICE and e.value.detail & M.MORI_DEV_HOST_ADDR
+    finally:
+        tp.close()
