@@ -269,6 +269,24 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     return;
   }
 
+  // Incremental keys: the listing group moves down from the top bits to just
+  // above the highest bit any program's priority uses (the same order), so the
+  // radix sort spends no pass on the bits between.  OR and AND of the keys
+  // follow, as the fields do not overlap.
+  uint32_t gshift = GROUP_SHIFT;
+  uint64_t kor = s_or, kand = s_and;
+  if (incremental) {
+    constexpr uint64_t SUB = (1ull << GROUP_SHIFT) - 1;
+    const uint64_t sub_or = kor & SUB;
+    gshift = sub_or ? 64u - (uint32_t)__clzll(sub_or) : 0u;
+    auto pack = [&](uint64_t k) { return ((k >> GROUP_SHIFT) << gshift) | (k & SUB); };
+#pragma unroll
+    for (int it = 0; it < IPT; ++it)
+      if (it * RT + tid < (int)P) key[it] = pack(key[it]);
+    kor = pack(kor);
+    kand = pack(kand);
+  }
+
   // ---- 2. stable sort of (key, id) ---------------------------------------
   if constexpr (IPT == 1 && RT <= 256) {
     // P <= 256: each program's rank is the number of programs before it in
@@ -311,7 +329,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     // Digits on which every real key agrees are skipped; padding keeps the
     // tail.  Five barriers a pass: counts, wave totals, bases, scatter, and the
     // read-back that also clears the next pass's counters.
-    const uint64_t varying = s_or ^ s_and;
+    const uint64_t varying = kor ^ kand;
     const uint64_t lanemask_lt = (1ull << lane) - 1ull;
     int last_shift = -1;
     for (int shift = 0; shift < KEY_BITS; shift += RADIX_BITS)
@@ -416,10 +434,11 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
 #pragma unroll
     for (int it = 0; it < IPT; ++it) {
       const uint32_t r = it * RT + tid;
-      const uint32_t g = r < P ? (uint32_t)(key[it] >> GROUP_SHIFT) : 5u;
+      const uint32_t g = r < P ? (uint32_t)(key[it] >> gshift) : 5u;
+      const uint64_t sub = gshift ? key[it] & ((1ull << gshift) - 1) : 0ull;  // priority: Acting bit 31
 #pragma unroll
       for (int j = 0; j < 5; ++j) gc[j] += g == (uint32_t)j;
-      cr += g == MORI_TIER_CPU && !((key[it] >> 31) & 1u);
+      cr += g == MORI_TIER_CPU && !((sub >> 31) & 1u);
     }
 #pragma unroll
     for (int j = 0; j < 5; ++j) add_to(&s_grp[j], gc[j]);
