@@ -633,3 +633,31 @@ def test_plans_supersede_without_swaps():
         assert e.value.code == M.MORI_EDEVICE and e.value.detail & M.MORI_DEV_HOST_ADDR
     finally:
         tp.close()
+
+
+@pytest.mark.parametrize("P", [255, 256, 257, 1023, 1024, 1025, 4095, 4096])
+def test_program_counts_at_the_shape_switches(P):
+    """Program counts on both sides of each switch between the rank kernel's
+    shapes (direct rank counting up to 256, one item per thread up to 1024,
+    four above): boundary, incremental and skip-fit plans, two steps each, with
+    exact ties, equal to the oracle."""
+    rng = np.random.default_rng(P)
+    geom = Geometry(layers=1, planes=2, block_tokens=1, row_bytes=16, num_blocks=0)
+    inst = random_instance(rng, P=P, max_blocks=4, geom=geom, extra_free=int(rng.integers(1, 100)), ties=True)
+    pair = Pair(inst, seed=P)
+    try:
+        bb = inst.geom.block_bytes
+        status = rng.integers(0, 3, P).astype(np.uint8)
+        for step, flags in enumerate((0, M.MORI_F_INCREMENTAL, M.MORI_F_SKIP_FIT | M.MORI_F_STATUS_KEY)):
+            kw = dict(gpu_bytes=int(rng.integers(0, inst.geom.num_blocks + 1)) * bb,
+                      cpu_bytes=int(rng.integers(0, inst.total_bytes // bb + 1)) * bb, flags=flags,
+                      window=inst.window if step % 2 == 0 else inst.window[:, :, ::-1].copy(),
+                      mode=(M.MORI_COPY_KERNEL, M.MORI_COPY_CE)[step % 2])
+            if flags & (M.MORI_F_INCREMENTAL | M.MORI_F_STATUS_KEY):
+                kw["status"] = status
+            log(f"shape switch P={P} step={step} flags={flags}")
+            res, plan = pair.step(**kw)
+            assert res.rc == oracle.OK and plan is not None
+            status = np.where((status == 2) & (pair.tier != 2), 0, status).astype(np.uint8)
+    finally:
+        pair.close()
