@@ -6,7 +6,7 @@
 //            twice, none both owned and free, none out of range, no page held
 //            by a CPU/Waiting program), mark pages of programs leaving the
 //            GPU as released, record the old page of every swap-out block;
-//   count    per 1024-page tile: pages free before the step, released pages
+//   count    per 512-page tile: pages free before the step, released pages
 //            of dropped programs, released pages of swapped-out programs; a
 //            page that is neither free nor owned is a leak;
 //   scan     exclusive prefix over tiles, totals, capacity; the summary is
@@ -33,7 +33,7 @@ namespace mori {
 namespace {
 
 constexpr int WG = 256;
-constexpr uint32_t SCAN_IN_ASSIGN = 1024;  // tiles (2^20 pages): each assign workgroup reads 16 B per tile
+constexpr uint32_t SCAN_IN_ASSIGN = 1024;  // tiles (2^19 pages): each assign workgroup reads 16 B per tile
 
 // Largest p in [0, P) with off[p] <= e (so off[p] <= e < off[p+1] when e < off[P]).
 __device__ inline uint32_t find_program(const uint32_t* off, uint32_t P, uint32_t e) {

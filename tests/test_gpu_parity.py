@@ -532,9 +532,9 @@ def test_two_contexts_on_two_host_threads():
             pair.close()
 
 
-@pytest.mark.parametrize("target", [1 << 20, (1 << 20) + 1, 1_500_000])
+@pytest.mark.parametrize("target", [1 << 19, (1 << 19) + 1, 1_500_000])
 def test_pools_around_the_tile_scan_switch(target):
-    """Pools of 2^20 pages (1024 tiles of 1024 pages: each page-assignment
+    """Pools of 2^19 pages (1024 tiles of 512 pages: each page-assignment
     workgroup scans the tile counts itself), one page more (1025 tiles: the
     tile scan is a kernel of its own) and 1.5 M pages, about 85% of them owned,
     so free pages, released pages and incoming slots span many tiles and
