@@ -30,8 +30,9 @@
 namespace mori {
 namespace {
 
-// Three shapes, chosen by P at launch: 256 threads x 1 item for P <= 256
-// (barriers over 4 waves; ranks counted directly), 1024 x 1 up to 1024 and
+// Four shapes, chosen by P at launch: one wave (64 threads, so every barrier
+// is a single wave's) for P <= 64, 256 threads x 1 item up to 256 (ranks
+// counted directly in both), 1024 x 1 up to 1024 and
 // 1024 threads x 4 items (striped: item x = it * RT + tid) up to 4096; fewer
 // item slices mean fewer ballots per radix pass.
 constexpr int RADIX_BITS = 8;
@@ -752,7 +753,8 @@ hipError_t launch_rank(const PlanArgs& a, hipStream_t s) {
     const uint64_t g = ((uint64_t)a.NB + 4ull * rt - 1) / (4ull * rt);
     return dim3(1 + (uint32_t)(g < 1024 ? g : 1024));
   };
-  if (a.P <= 256) hipLaunchKernelGGL((rank_partition_kernel<256, 1>), grid(256), dim3(256), 0, s, a);
+  if (a.P <= 64) hipLaunchKernelGGL((rank_partition_kernel<64, 1>), grid(64), dim3(64), 0, s, a);
+  else if (a.P <= 256) hipLaunchKernelGGL((rank_partition_kernel<256, 1>), grid(256), dim3(256), 0, s, a);
   else if (a.P <= 1024) hipLaunchKernelGGL((rank_partition_kernel<1024, 1>), grid(1024), dim3(1024), 0, s, a);
   else hipLaunchKernelGGL((rank_partition_kernel<1024, 4>), grid(1024), dim3(1024), 0, s, a);
   return hipGetLastError();
