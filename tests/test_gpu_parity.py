@@ -635,12 +635,12 @@ def test_plans_supersede_without_swaps():
         tp.close()
 
 
-@pytest.mark.parametrize("P", [255, 256, 257, 1023, 1024, 1025, 4095, 4096])
+@pytest.mark.parametrize("P", [63, 64, 65, 255, 256, 257, 1023, 1024, 1025, 4095, 4096])
 def test_program_counts_at_the_shape_switches(P):
     """Program counts on both sides of each switch between the rank kernel's
-    shapes (direct rank counting up to 256, one item per thread up to 1024,
-    four above): boundary, incremental and skip-fit plans, two steps each, with
-    exact ties, equal to the oracle."""
+    shapes (one wave up to 64 and 256 threads up to 256, both counting ranks
+    directly; one item per thread up to 1024, four above): boundary,
+    incremental and skip-fit plans with exact ties, equal to the oracle."""
     rng = np.random.default_rng(P)
     geom = Geometry(layers=1, planes=2, block_tokens=1, row_bytes=16, num_blocks=0)
     inst = random_instance(rng, P=P, max_blocks=4, geom=geom, extra_free=int(rng.integers(1, 100)), ties=True)
