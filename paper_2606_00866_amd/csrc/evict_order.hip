@@ -61,9 +61,10 @@ constexpr uint32_t SMALL_SORT = 1u << 19;
 inline int keys_per_thread(uint32_t N) { return N <= SMALL_SORT ? 4 : 8; }
 constexpr uint64_t TIME_LIMIT = 1ull << 62;
 constexpr uint32_t KEY_WG_MAX = 128;     // workgroups of the keys kernel at most (one digit-count set each)
-constexpr int KEYS_PER_ROUND = 4;        // keys per thread whose loads the keys kernel issues together
-                                         // (measured: 8 and 16 are 3 and 11 us slower at 69 938 blocks,
-                                         // 8 is 2.5 us faster at 2^20)
+// Keys per thread whose loads the keys kernel issues together: 4 for the
+// look-back passes, 8 above (measured: 8 and 16 are 3 and 11 us slower at
+// 69 938 blocks, 8 is 2.5 us faster at 2^20).
+constexpr int KEYS_PER_ROUND_SMALL = 4, KEYS_PER_ROUND_LARGE = 8;
 constexpr uint32_t TOT_SPLIT = 8;        // totals: workgroups per pass, each summing a share of the sets
 // Tile counts up to this use one look-back kernel per pass, more use three
 // kernels (histogram, per-digit scan, scatter): each look-back round is a
@@ -116,6 +117,7 @@ __global__ __launch_bounds__(ET) void evict_init_kernel(EvictArgs a) {
   }
 }
 
+template <int KEYS_PER_ROUND>
 __global__ __launch_bounds__(ET) void evict_keys_kernel(EvictArgs a) {
   // position of each type label in the tier's eviction order (busy, idle, inactive)
   const uint32_t gpu_pos[3] = {2, 1, 0}, cpu_pos[3] = {1, 2, 0};
@@ -779,7 +781,8 @@ hipError_t launch_evict(uint32_t N, const uint8_t* type, const uint64_t* last_ac
   const uint32_t tiles = a.ntiles ? a.ntiles : 1;
   hipLaunchKernelGGL(evict_init_kernel, dim3(tiles < 256 ? tiles : 256), dim3(ET), 0, s, a);
   a.key_wg = tiles < KEY_WG_MAX ? tiles : KEY_WG_MAX;
-  hipLaunchKernelGGL(evict_keys_kernel, dim3(a.key_wg), dim3(ET), 0, s, a);
+  if (a.onesweep) hipLaunchKernelGGL(evict_keys_kernel<KEYS_PER_ROUND_SMALL>, dim3(a.key_wg), dim3(ET), 0, s, a);
+  else hipLaunchKernelGGL(evict_keys_kernel<KEYS_PER_ROUND_LARGE>, dim3(a.key_wg), dim3(ET), 0, s, a);
   if (a.onesweep) hipLaunchKernelGGL(evict_totals_kernel, dim3(8 * TOT_SPLIT), dim3(ET), 0, s, a);
   if (a.ntiles) {
     if (kpt == 4) launch_tiles<4>(a, s);
