@@ -174,7 +174,7 @@ typedef struct {
   uint64_t pages_out, pages_in, pages_admit;
   uint64_t pages_free_before, pages_released, pages_recycled, pages_free_after;
   uint64_t bytes_out, bytes_in, gpu_bytes_after, cpu_bytes_after, ssd_bytes_after;
-  uint64_t pages_dropped; /* released pages of programs dropped to Waiting (nothing reads them) */
+  uint64_t pages_dropped; /* released pages of idle programs dropped to Waiting (nothing uses them) */
   const uint32_t* order;        /* [P] program ids, busiest first (incremental: see below) */
   const uint64_t* prefix;       /* [P] inclusive KV-byte prefix in rank order */
   const uint8_t* tier_old;      /* [P] */
@@ -190,16 +190,23 @@ typedef struct {
  * MORI_MAX_PROGRAMS bounds P of every later call.  staging_bytes is the
  * device staging of copy-engine swaps per direction (0: 512 MiB), used as two
  * halves of whole runs (it must hold at least two runs); copy-engine swaps
- * move the bytes in chunks of one half.  When the process has at least 8
- * hardware queues (GPU_MAX_HW_QUEUES >= 8 when HIP starts), the context also
- * owns one copy stream per direction, so the copy engines drain one half while
- * the gather/scatter kernel works on the other; with fewer queues those
- * streams would share queues with the caller's and serialise the directions,
- * and the copies run on the caller's stream instead.  The two streams given
- * to the swaps should be distinct and created early (streams beyond the
- * queue count share queues).  *out is set on success.
- * EINVAL: null pool/out, bad geometry or alignment; EHIP: allocation. */
-int mori_create(const mori_pool* pool, uint32_t max_programs, uint64_t staging_bytes, mori_ctx** out);
+ * move the bytes in chunks of one half.  flags:
+ *   MORI_CREATE_COPY_STREAMS  the context owns one copy stream per direction,
+ *     so the copy engines drain one staging half while the gather/scatter
+ *     kernel works on the other.  HIP maps a process's streams onto
+ *     GPU_MAX_HW_QUEUES hardware queues (4 by default, read when HIP starts)
+ *     and streams beyond that share queues, where one stream's waits block
+ *     the other's work and the two swap directions serialise; set the flag
+ *     only when the process has at least 8 queues (the two swap streams, the
+ *     two copy streams).  Without it the copies run on the caller's stream,
+ *     in order with the kernels.
+ * The two streams given to the swaps should be distinct and created early
+ * (streams beyond the queue count share queues).  *out is set on success.
+ * EINVAL: null pool/out, unknown flags, bad geometry or alignment; EHIP:
+ * allocation. */
+#define MORI_CREATE_COPY_STREAMS 1u
+int mori_create(const mori_pool* pool, uint32_t max_programs, uint64_t staging_bytes, uint32_t flags,
+                mori_ctx** out);
 
 /* Waits for the context's outstanding work and frees it.  NULL is a no-op. */
 int mori_destroy(mori_ctx* ctx);
@@ -224,13 +231,21 @@ int mori_host_free(void* ptr);
  * mori_plan_wait.
  *
  * Pages for programs entering the GPU are handed out in this order: pages
- * free before the step, then pages of programs dropped to Waiting (nothing
- * reads them), then pages of swapped-out programs (free once the swap-out has
- * read them), each group in ascending page id; programs promoted from a lower
- * tier take them first, then programs admitted from Waiting, each group in
- * rank order, blocks in logical order.  A slot at or past pages_free_before +
- * pages_dropped is on a page the swap-out reads: the swap-in waits for the
- * swap-out before writing it, and the caller before prefilling it.
+ * free before the step; then pages of programs dropped to Waiting that
+ * nothing uses any more; then, together, pages of swapped-out programs (free
+ * once the swap-out has read them) and pages of programs dropped while they
+ * may still be running an inference step (free once that step has ended);
+ * each group in ascending page id.  A dropped program counts as running when
+ * the plan reads statuses (MORI_F_STATUS_KEY or MORI_F_INCREMENTAL) and its
+ * status is not MORI_ST_ACTING (Sec. 4.3.1 demotes a Reasoning victim lazily:
+ * its current step is not interrupted); without statuses the caller vouches
+ * that dropped programs are idle.  The caller orders such a program's current
+ * step before mori_kv_swap_out on the swap-out stream.  Programs promoted
+ * from a lower tier take the pages first, then programs admitted from
+ * Waiting, each group in rank order, blocks in logical order.  A slot at or
+ * past pages_free_before + pages_dropped is on a page still in use: the
+ * swap-in waits for the swap-out stream before writing it, and the caller
+ * (MORI_Q_OUT_EVENT) before prefilling it.
  *
  * Default policy (Sec. 4.3, Sec. 7.2): rank all programs by idleness (Eq. 1),
  * busiest first, and fill the GPU tier, then the CPU tier, from the busiest
@@ -243,7 +258,8 @@ int mori_host_free(void* ptr);
  * (2) While the GPU tier exceeds its budget, the next program in demotion
  * order leaves it, to the CPU tier if it fits in the CPU room left, else to
  * Waiting; a Reasoning victim is demoted lazily: the caller lets its current
- * inference step finish (orders it before the swap-out on the swap stream).
+ * inference step finish (orders it before the swap-out on the swap-out
+ * stream), and its pages are handed out only after that (see above).
  * (3) The GPU room left is filled from, in order: CPU programs waiting for
  * inference, returning Waiting programs waiting for inference, new arrivals
  * smallest context first; lowest idleness first within a level, ties lowest
@@ -294,9 +310,10 @@ int mori_kv_swap_out(mori_ctx* ctx, const uint64_t* host_dst, uint32_t mode, voi
 /* Swap-in of the last plan: for every program p with category IN, copies
  * host_src[p] + (q * nblk_p + i) * run_bytes into its newly allocated page of
  * block i, plane q.  Waits (on the stream) for the plan and, before writing a
- * page that the swap-out of the same plan reads, for that swap-out (pages
- * free before the step and pages of dropped programs need no wait).  The host
- * buffers may be reused after it completes.  ESTATE: no plan, swap-in already
+ * page that is still in use (the swap-out of the same plan reads it, or a
+ * dropped program's step ordered before that swap-out uses it), for that
+ * swap-out (pages free before the step and pages of idle dropped programs
+ * need no wait).  The host buffers may be reused after it completes.  ESTATE: no plan, swap-in already
  * enqueued, or swap-out of the plan not yet enqueued. */
 int mori_kv_swap_in(mori_ctx* ctx, const uint64_t* host_src, uint32_t mode, void* stream);
 

@@ -359,7 +359,7 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
   uint64_t* prefix = (uint64_t*)malloc(sizeof(uint64_t) * np);
   uint8_t* tier_new = (uint8_t*)malloc(np);
   uint8_t* cat = (uint8_t*)malloc(np);
-  uint8_t* page_state = (uint8_t*)calloc(NB ? NB : 1, 1); /* bit0 free, bit1 owned, bit2 released */
+  uint8_t* page_state = (uint8_t*)calloc(NB ? NB : 1, 1); /* bit0 free, bit1 owned, bit2 released, bit3 free only later */
   uint32_t* pages_avail = (uint32_t*)malloc(sizeof(uint32_t) * (NB ? NB : 1));
   uint32_t* new_tbl = NULL;
 
@@ -399,6 +399,17 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
   if (rc == ORC_OK)
     for (uint32_t p = 0; p < P; ++p) cat[p] = orc_category(tier[p], tier_new[p]);
 
+  /* -- which programs dropped from the GPU may still be using their pages.
+        Reading (Sec. 4.3.1, lazy demotion): a Reasoning victim is not
+        interrupted; its current inference step ends first, so its pages are
+        not free at once.  When the plan reads statuses (ORC_F_STATUS_KEY or
+        ORC_F_INCREMENTAL), every status other than Acting counts as running
+        (a new arrival found on the GPU counts as Reasoning); without
+        statuses the caller vouches that dropped programs are idle. -- */
+  uint8_t* may_run = (uint8_t*)calloc(np, 1);
+  if (rc == ORC_OK && status != NULL && (flags & (ORC_F_STATUS_KEY | ORC_F_INCREMENTAL)))
+    for (uint32_t p = 0; p < P; ++p) may_run[p] = status[p] != ORC_ST_ACTING;
+
   /* -- pool consistency: every page is either free or owned by exactly one
         GPU-resident program; non-resident programs hold no page -- */
   if (rc == ORC_OK) {
@@ -416,7 +427,8 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
           continue;
         }
         page_state[pg] |= 2u;
-        if (cat[p] == ORC_DROP_GPU) page_state[pg] |= 4u;      /* released, nothing to read */
+        if (cat[p] == ORC_DROP_GPU && !may_run[p]) page_state[pg] |= 4u; /* released, nothing reads it */
+        if (cat[p] == ORC_DROP_GPU && may_run[p]) page_state[pg] |= 4u | 8u; /* free once its step ended */
         if (cat[p] == ORC_OUT) page_state[pg] |= 4u | 8u;      /* released once the swap-out read it */
       }
     }
@@ -430,12 +442,14 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
 
   /* -- step 4: page allocation (Reading: pages free before this step in
         ascending id order, then the pages of programs dropped from the GPU to
-        Waiting (nothing reads them), then the pages of programs swapped out
-        (free once the swap-out has read them), each group in ascending id
-        order; they are handed out first to the programs promoted from a lower
-        tier, then to those admitted from Waiting, following the promotion
-        priority of Sec. 4.3.1, each group in rank order, each program's
-        blocks in logical order) -- */
+        Waiting that nothing reads any more, then the pages that are free only
+        later -- those of programs swapped out (once the swap-out has read
+        them) and those of dropped programs that may still be running (once
+        their step has ended) -- together in ascending id order; they are
+        handed out first to the programs promoted from a lower tier, then to
+        those admitted from Waiting, following the promotion priority of
+        Sec. 4.3.1, each group in rank order, each program's blocks in logical
+        order) -- */
   uint64_t n_free0 = 0, n_rel = 0, n_drop = 0, need = 0;
   if (rc == ORC_OK) {
     for (uint32_t pg = 0; pg < NB; ++pg)
@@ -537,6 +551,7 @@ int orc_rebalance(const orc_geometry* g, uint8_t* pool_bytes, uint32_t P, uint32
   free(tier_new);
   free(cat);
   free(page_state);
+  free(may_run);
   free(pages_avail);
   free(new_tbl);
   return rc;

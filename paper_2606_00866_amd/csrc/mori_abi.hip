@@ -11,8 +11,10 @@
 //              the context's copy stream, while the next gather fills the
 //              other half.
 //   swap-in    direct: translate -> scatter of slots on pages free before the
-//              step or released by dropped programs -> wait for the swap-out ->
-//              scatter of slots on pages it has read; copy engine: per chunk,
+//              step or released by idle dropped programs -> wait for the
+//              swap-out -> scatter of slots on pages that were still in use
+//              (read by the swap-out, or by a dropped program's inference step
+//              ordered before it); copy engine: per chunk,
 //              hipMemcpyAsync host -> staging half on the copy stream -> scatter
 //              kernel on the caller's stream (after the swap-out event from the
 //              first chunk that writes a page the swap-out reads), the next
@@ -21,7 +23,6 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -36,15 +37,6 @@ constexpr uint64_t kDefaultStaging = 512ull << 20;
 constexpr uint32_t kGridHost = 128;     // enough outstanding 16-B accesses to fill the host link
 constexpr uint32_t kGridDevice = 8192;  // HBM-to-HBM gathers and scatters
 constexpr uint64_t kTimeOnly = ~0ull;
-constexpr int kQueuesForCopyStreams = 8;
-
-// Hardware queues per process that HIP will create (its default is 4).
-int hw_queues() {
-  const char* v = std::getenv("GPU_MAX_HW_QUEUES");
-  if (!v || !*v) return 4;
-  const int n = std::atoi(v);
-  return n > 0 ? n : 4;
-}
 
 struct BlobLayout {
   size_t sum, order, prefix, tier_old, tier_new, cat, out_prog, in_prog, out_base, in_base, total;
@@ -92,7 +84,7 @@ struct mori_ctx {
   uint64_t* tile_base = nullptr;
   uint64_t* addr_stage[2] = {nullptr, nullptr};
   uint64_t* addr_dev[2] = {nullptr, nullptr};
-  uint32_t* swap_err = nullptr;
+  uint32_t* swap_err = nullptr;  // [2] per direction
   DevRange* ranges_dev = nullptr;
   uint64_t* addr_pinned = nullptr;  // [2][max_programs]
   uint8_t* staging[2] = {nullptr, nullptr};  // per direction, two halves
@@ -188,9 +180,11 @@ static void free_ctx(mori_ctx* c) {
   delete c;
 }
 
-extern "C" int mori_create(const mori_pool* pool, uint32_t max_programs, uint64_t staging_bytes, mori_ctx** out) {
+extern "C" int mori_create(const mori_pool* pool, uint32_t max_programs, uint64_t staging_bytes, uint32_t flags,
+                           mori_ctx** out) {
   if (!pool || !out) return MORI_EINVAL;
   *out = nullptr;
+  if (flags & ~MORI_CREATE_COPY_STREAMS) return MORI_EINVAL;
   if (!pool->base || (reinterpret_cast<uintptr_t>(pool->base) & 255u)) return MORI_EINVAL;
   if (!pool->layers || !pool->planes || !pool->block_tokens || !pool->row_bytes || (pool->row_bytes & 15u))
     return MORI_EINVAL;
@@ -238,7 +232,7 @@ extern "C" int mori_create(const mori_pool* pool, uint32_t max_programs, uint64_
   const size_t o_base = take(4 * pm), o_pstate = take(4 * NB), o_out_src = take(4 * NB), o_in_dst = take(4 * NB);
   const size_t o_tc = take(16ull * c->ntiles), o_tb = take(16ull * c->ntiles);
   const size_t o_as0 = take(8 * pm), o_as1 = take(8 * pm), o_ad0 = take(8 * pm), o_ad1 = take(8 * pm);
-  const size_t o_err = take(4), o_rng = take(sizeof(DevRange) * MORI_MAX_RANGES);
+  const size_t o_err = take(8), o_rng = take(sizeof(DevRange) * MORI_MAX_RANGES);
   if ((e = hipMalloc(&c->scratch, o)) != hipSuccess) return fail(e);
   c->base = reinterpret_cast<uint32_t*>(c->scratch + o_base);
   c->pstate = reinterpret_cast<uint32_t*>(c->scratch + o_pstate);
@@ -262,12 +256,13 @@ extern "C" int mori_create(const mori_pool* pool, uint32_t max_programs, uint64_
                          &c->ev_half_ready[1][0], &c->ev_half_ready[1][1], &c->ev_half_free[0][0],
                          &c->ev_half_free[0][1], &c->ev_half_free[1][0], &c->ev_half_free[1][1]})
     if ((e = hipEventCreateWithFlags(ev, hipEventDisableTiming)) != hipSuccess) return fail(e);
-  // Copy streams (default priority) only when the process has hardware queues
-  // to spare: HIP maps streams onto GPU_MAX_HW_QUEUES queues (4 by default) and
-  // streams beyond that share a queue, where each stream's waits block the
-  // other's work and the two swap directions serialise.  Without them the
-  // copies run on the caller's stream, in order with the gathers/scatters.
-  if (hw_queues() >= kQueuesForCopyStreams)
+  // Copy streams (default priority) only when the caller says the process has
+  // hardware queues to spare: HIP maps streams onto GPU_MAX_HW_QUEUES queues
+  // (4 by default) and streams beyond that share a queue, where each stream's
+  // waits block the other's work and the two swap directions serialise.
+  // Without them the copies run on the caller's stream, in order with the
+  // gathers/scatters.
+  if (flags & MORI_CREATE_COPY_STREAMS)
     for (int d = 0; d < 2; ++d)
       if ((e = hipStreamCreateWithFlags(&c->cstream[d], hipStreamNonBlocking)) != hipSuccess) return fail(e);
   *out = c;
@@ -672,8 +667,9 @@ extern "C" int mori_kv_swap_in(mori_ctx* ctx, const uint64_t* host_src, uint32_t
     const uint32_t* base = ctx->host<uint32_t>(ctx->L.in_base);
     if (!host_check(ctx, host_src, progs, n, base)) return MORI_EINVAL;
     HIP_TRY(ctx, hipStreamWaitEvent(s, ctx->ev_plan, 0));
-    // slots below `ready` are on pages free before the step or released by a
-    // dropped program; the rest are on pages the swap-out reads first
+    // slots below `ready` are on pages free before the step or released by an
+    // idle dropped program; the rest are on pages still in use until the
+    // swap-out stream has passed
     const uint64_t LC = ctx->LC, run = ctx->run, ready = sh->pages_free_before + sh->pages_dropped;
     const uint64_t total = n ? (uint64_t)base[n] * LC : 0;
     const uint64_t cu = ctx->staging_bytes / 2 / run;  // chunk = one staging half
@@ -740,9 +736,9 @@ extern "C" int mori_query(mori_ctx* ctx, int what, uint64_t* value) {
       if (ctx->have_plan) HIP_TRY(ctx, hipEventSynchronize(ctx->ev_plan));
       if (ctx->out_recorded) HIP_TRY(ctx, hipEventSynchronize(ctx->ev_out));
       if (ctx->in_recorded) HIP_TRY(ctx, hipEventSynchronize(ctx->ev_in));
-      uint32_t swap_err = 0;
-      HIP_TRY(ctx, hipMemcpy(&swap_err, ctx->swap_err, sizeof swap_err, hipMemcpyDeviceToHost));
-      *value = (uint64_t)(ctx->have_plan ? ctx->sum_host()->error : 0u) | swap_err;
+      uint32_t swap_err[2] = {0, 0};
+      HIP_TRY(ctx, hipMemcpy(swap_err, ctx->swap_err, sizeof swap_err, hipMemcpyDeviceToHost));
+      *value = (uint64_t)(ctx->have_plan ? ctx->sum_host()->error : 0u) | swap_err[0] | swap_err[1];
       return MORI_OK;
     }
     case MORI_Q_LAST_MODE:

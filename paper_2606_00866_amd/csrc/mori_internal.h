@@ -12,7 +12,8 @@ namespace mori {
 constexpr uint32_t PS_FREE = 1u;   // marked free in the caller's free map before the step
 constexpr uint32_t PS_OWNED = 2u;  // owned by a GPU-resident program
 constexpr uint32_t PS_REL = 4u;    // owned by a program leaving the GPU this step
-constexpr uint32_t PS_COPY = 8u;   // ... whose KV the swap-out reads from it first
+constexpr uint32_t PS_LATER = 8u;  // ... and free only after the swap-out stream has passed: the
+                                   // swap-out reads it, or its dropped program may still be running
 
 constexpr int PAGE_TILE = 512;     // pages per workgroup in the page-allocation kernels (2 per thread;
                                    // measured: 0.5-1 us faster per plan than 1024, 2048 slower)
@@ -27,7 +28,7 @@ struct DevSummary {
   uint64_t pages_free_before, pages_released, pages_recycled, pages_free_after;
   uint64_t bytes_out, bytes_in, gpu_bytes_after, cpu_bytes_after, ssd_bytes_after;
   uint64_t need;  // pages_in + pages_admit
-  uint64_t pages_dropped;  // released pages nothing reads: slots below free-before + this need no wait
+  uint64_t pages_dropped;  // released pages nothing reads any more: slots below free-before + this need no wait
 };
 
 // A registered memory range usable by the swap kernels.
@@ -66,9 +67,9 @@ struct PlanArgs {
   uint32_t* pstate;       // [NB]
   uint32_t* out_src;      // [pages_out] old page of each out page index
   uint32_t* in_dst;       // [need] page of each slot
-  uint64_t* tile_cnt;     // [2 ntiles]: packed (free-before, dropped << 32), then swapped-out counts
+  uint64_t* tile_cnt;     // [2 ntiles]: packed (free-before, dropped << 32), then free-later counts
   uint64_t* tile_base;    // [2 ntiles] exclusive prefixes of both halves of tile_cnt
-  uint32_t* swap_err;     // cleared by every plan
+  uint32_t* swap_err;     // [2] swap-out, swap-in address errors; cleared by every plan
   // The pinned host mirror of the plan blob, as the device addresses it: the
   // kernels that finish a part of the plan store it there too, so no copy of
   // the blob follows the plan.  Mirror address = blob address + host_delta.
@@ -90,7 +91,7 @@ struct SwapArgs {
   const uint32_t* pg_base;  // out_pg_base or in_pg_base
   const uint32_t* pages;    // out_src (by out-page index) or in_dst (by slot)
   const uint64_t* addr;     // device address of each program's host buffer
-  const uint32_t* swap_err;
+  const uint32_t* swap_err; // [2] address errors found by the swap-out's and the swap-in's translation
   uint8_t* staging;         // non-null: chunk staging buffer (copy-engine mode)
   uint64_t u_begin, u_end;  // staging mode: unit range of the chunk
   uint32_t part;            // swap-in: 0 all slots, 1 slots < free-before, 2 slots >= free-before
@@ -106,7 +107,7 @@ struct TranslateArgs {
   uint64_t* addr_out;       // [P] translated device addresses
   const DevRange* ranges;
   uint32_t nranges;
-  uint32_t* swap_err;
+  uint32_t* swap_err;       // [2]: this direction's word is swap_err[dir_in]
 };
 
 // launchers (return the launch error)

@@ -7,18 +7,23 @@
 //            by a CPU/Waiting program), mark pages of programs leaving the
 //            GPU as released, record the old page of every swap-out block;
 //   count    per 512-page tile: pages free before the step, released pages
-//            of dropped programs, released pages of swapped-out programs; a
-//            page that is neither free nor owned is a leak;
+//            free at once (programs dropped to Waiting that are idle) and
+//            released pages free only later (programs swapped out, and
+//            programs dropped while they may still run an inference step:
+//            Sec. 4.3.1 demotes a Reasoning victim lazily, so its step goes
+//            on reading and appending to its pages); a page that is neither
+//            free nor owned is a leak;
 //   scan     exclusive prefix over tiles, totals, capacity; the summary is
 //            final here and is stored into the host mirror.  Up to
 //            SCAN_IN_ASSIGN tiles every assign workgroup does this itself
 //            from the tile counts (one launch fewer); above, one workgroup
 //            of a kernel of its own;
 //   assign   slot j of the incoming programs takes the j-th page of
-//            (free-before ++ dropped ++ swapped out, each ascending): pages
-//            nothing reads come before pages the swap-out reads, so the
-//            swap-in waits only for slots past the first two groups; the free
-//            map after the step is what is left of that sequence;
+//            (free-before ++ free at once ++ free later, each ascending):
+//            pages nothing uses come before pages still in use, so the
+//            swap-in waits for the swap-out stream only for slots past the
+//            first two groups; the free map after the step is what is left
+//            of that sequence;
 //   commit   rewrite the block tables (released -> no page, incoming -> their
 //            slots' pages) and the tier vector.
 //
@@ -63,7 +68,13 @@ __global__ __launch_bounds__(WG) void pages_claim_kernel(PlanArgs a) {
       continue;
     }
     const uint8_t c = a.cat[p];
-    const uint32_t leaves = c == MORI_CAT_OUT ? (PS_REL | PS_COPY) : c == MORI_CAT_DROP_GPU ? PS_REL : 0u;
+    // a program dropped while it may still run (with statuses: anything but
+    // Acting) frees its pages only after its step, which the caller orders
+    // before the swap-out on the swap-out stream
+    const bool running = c == MORI_CAT_DROP_GPU && (a.flags & (MORI_F_STATUS_KEY | MORI_F_INCREMENTAL)) &&
+                         a.status[p] != MORI_ST_ACTING;
+    const uint32_t leaves =
+        c == MORI_CAT_OUT || running ? (PS_REL | PS_LATER) : c == MORI_CAT_DROP_GPU ? PS_REL : 0u;
     const uint32_t old = atomicOr(&a.pstate[pg], PS_OWNED | leaves);
     if (old & (PS_FREE | PS_OWNED)) err |= MORI_DEV_PAGE_DUP;
     if (c == MORI_CAT_OUT) {
@@ -88,7 +99,7 @@ __global__ __launch_bounds__(WG) void pages_count_kernel(PlanArgs a) {
     if (pg >= a.NB) break;
     const uint32_t st = a.pstate[pg];
     if (st == PS_FREE) ++nf;
-    else if (st & PS_COPY) ++nc;
+    else if (st & PS_LATER) ++nc;
     else if (st & PS_REL) ++nd;
     else if (st == 0) err |= MORI_DEV_PAGE_LEAK;
   }
@@ -151,7 +162,7 @@ __global__ __launch_bounds__(1024) void pages_scan_kernel(PlanArgs a) {
     return;
   }
   uint64_t carry[2] = {0, 0};
-  for (int half = 0; half < 2; ++half) {  // (free-before | dropped << 32), then swapped out
+  for (int half = 0; half < 2; ++half) {  // (free-before | dropped << 32), then free later
     const uint64_t* cnt = a.tile_cnt + (uint64_t)half * a.ntiles;
     uint64_t* out = a.tile_base + (uint64_t)half * a.ntiles;
     for (uint32_t t0 = 0; t0 < a.ntiles; t0 += 1024) {
@@ -180,7 +191,7 @@ __global__ __launch_bounds__(WG) void pages_assign_kernel(PlanArgs a) {
   const uint64_t need = a.sum->need;
   uint64_t tb, tbc, nf_all, nd_all;
   if constexpr (SCAN) {
-    uint64_t v[4] = {0, 0, 0, 0};  // prefix (free | dropped << 32), prefix swapped-out, and the totals
+    uint64_t v[4] = {0, 0, 0, 0};  // prefix (free | dropped << 32), prefix free-later, and the totals
     for (uint32_t t = threadIdx.x; t < a.ntiles; t += WG) {
       const uint64_t c0 = a.tile_cnt[t], c1 = a.tile_cnt[a.ntiles + t];
       if (t < blockIdx.x) v[0] += c0, v[1] += c1;
@@ -220,7 +231,7 @@ __global__ __launch_bounds__(WG) void pages_assign_kernel(PlanArgs a) {
     const uint64_t pg = start + j;
     st[j] = pg < a.NB ? a.pstate[pg] : PS_OWNED;
     if (st[j] == PS_FREE) ++nf;
-    else if (st[j] & PS_COPY) ++nc;
+    else if (st[j] & PS_LATER) ++nc;
     else if (st[j] & PS_REL) ++nd;
   }
   uint64_t tot;
@@ -234,7 +245,7 @@ __global__ __launch_bounds__(WG) void pages_assign_kernel(PlanArgs a) {
     const uint64_t pg = start + j;
     uint64_t slot;
     if (st[j] == PS_FREE) slot = fi++;
-    else if (st[j] & PS_COPY) slot = nf_all + nd_all + ci++;
+    else if (st[j] & PS_LATER) slot = nf_all + nd_all + ci++;
     else if (st[j] & PS_REL) slot = nf_all + di++;
     else continue;
     if (slot < need) {
@@ -287,7 +298,7 @@ __global__ __launch_bounds__(WG) void translate_kernel(TranslateArgs t) {
     if (!ok) err |= MORI_DEV_HOST_ADDR;
     t.addr_out[p] = dev;
   }
-  if (err) atomicOr(t.swap_err, err);
+  if (err) atomicOr(&t.swap_err[t.dir_in], err);
 }
 
 inline uint32_t grid_for(uint64_t n, uint32_t cap) {

@@ -265,7 +265,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
       z.error = s_err;
       *a.sum = z;
       *host_mirror(a, a.sum) = z;
-      *a.swap_err = 0;
+      a.swap_err[0] = a.swap_err[1] = 0;
     }
     return;
   }
@@ -740,7 +740,7 @@ __global__ __launch_bounds__(RT) void rank_partition_kernel(PlanArgs a) {
     z.ssd_bytes_after = s_ssd_after;
     z.need = (uint64_t)pages_in + pages_admit;
     *a.sum = z;
-    *a.swap_err = 0;
+    a.swap_err[0] = a.swap_err[1] = 0;
   }
 }
 

@@ -18,11 +18,13 @@
 //   swap_in  : host buffer (direct) or staging -> newly allocated pool page
 //
 // Swap-in is launched in two parts in direct mode: slots taken from pages
-// that were free before the step or released by programs dropped to Waiting,
-// which no swap-out reads, and slots taken from pages of swapped-out
-// programs, which must wait for the swap-out (the host orders the second part
-// after the swap-out's completion event).  Page allocation hands out the
-// first kind first, so the split is one slot index.
+// that were free before the step or released by idle programs dropped to
+// Waiting, which nothing uses any more, and slots taken from pages that are
+// free only once the swap-out stream has passed (pages the swap-out reads,
+// and pages of dropped programs whose inference step the caller orders
+// before the swap-out), which must wait for the swap-out (the host orders the
+// second part after the swap-out's completion event).  Page allocation hands
+// out the first kind first, so the split is one slot index.
 #include "mori_internal.h"
 
 namespace mori {
@@ -93,7 +95,7 @@ __device__ inline bool unit_range(const SwapArgs& s, uint32_t n, uint64_t* lo, u
     }
     *hi = (uint64_t)s.pg_base[a] * LC;
   } else if (!kOut && s.part == 2) {
-    if (s.pg_base[n] <= nf) return false;  // no slot reaches a page the swap-out reads
+    if (s.pg_base[n] <= nf) return false;  // no slot reaches a page that is free only later
     *lo = (uint64_t)s.pg_base[find_slice(s.pg_base, n, nf)] * LC;
   }
   return *lo < *hi;
@@ -145,7 +147,11 @@ __device__ inline bool unit_ends(const SwapArgs& s, Cursor& c, uint64_t u, uint6
 // PER runs per pass (runs_per_pass below, chosen on the host from the run size)
 template <bool kOut, uint32_t PER>
 __global__ __launch_bounds__(NT) void swap_kernel(SwapArgs s) {
-  if (s.sum->error || *s.swap_err) return;
+  // A swap-out stops on its own address errors only: the swap-in translates
+  // concurrently on the other stream.  A swap-in also stops on the swap-out's
+  // (ordered before it by the time it writes a page the swap-out reads): it
+  // must not overwrite pages whose KV a failed swap-out did not save.
+  if (s.sum->error || s.swap_err[0] || (!kOut && s.swap_err[1])) return;
   const uint32_t n = kOut ? s.sum->n_out : s.sum->n_in;
   uint64_t lo, hi;
   if (n == 0 || !unit_range<kOut>(s, n, &lo, &hi)) return;

@@ -24,6 +24,7 @@ MORI_NO_PAGE = 0xFFFFFFFF
 MORI_F_STATUS_KEY, MORI_F_SKIP_FIT, MORI_F_IDLENESS_GIVEN, MORI_F_INCREMENTAL, MORI_F_SSD_TIER = 1, 2, 4, 8, 16
 MORI_ST_REASONING, MORI_ST_ACTING, MORI_ST_NEW = 0, 1, 2
 MORI_COPY_AUTO, MORI_COPY_KERNEL, MORI_COPY_CE = 0, 1, 2
+MORI_CREATE_COPY_STREAMS = 1
 (MORI_CAT_KEPT, MORI_CAT_OUT, MORI_CAT_IN, MORI_CAT_DROP_GPU, MORI_CAT_DROP_CPU, MORI_CAT_ADMIT_GPU,
  MORI_CAT_ADMIT_CPU, MORI_CAT_CPU_SSD, MORI_CAT_SSD_CPU, MORI_CAT_DROP_SSD, MORI_CAT_ADMIT_SSD) = range(11)
 MORI_MAX_PROGRAMS, MORI_MAX_WINDOW, MORI_MAX_RANGES, MORI_MAX_REPLICAS = 4096, 64, 64, 1024
@@ -81,7 +82,7 @@ def lib():
             raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
         L = C.CDLL(LIB_PATH)
         V, U32, U64, I = C.c_void_p, C.c_uint32, C.c_uint64, C.c_int
-        L.mori_create.argtypes = [C.POINTER(mori_pool), U32, U64, C.POINTER(V)]
+        L.mori_create.argtypes = [C.POINTER(mori_pool), U32, U64, U32, C.POINTER(V)]
         L.mori_destroy.argtypes = [V]
         L.mori_register.argtypes = [V, V, U64]
         L.mori_host_alloc.argtypes = [U64, C.POINTER(V)]
@@ -105,9 +106,9 @@ def lib():
     return _lib
 
 
-def mori_create(pool: mori_pool, max_programs: int, staging_bytes: int = 0):
+def mori_create(pool: mori_pool, max_programs: int, staging_bytes: int = 0, flags: int = 0):
     ctx = C.c_void_p()
-    rc = lib().mori_create(C.byref(pool), max_programs, staging_bytes, C.byref(ctx))
+    rc = lib().mori_create(C.byref(pool), max_programs, staging_bytes, flags, C.byref(ctx))
     return rc, ctx
 
 

@@ -10,6 +10,7 @@ from __future__ import annotations
 
 import bisect
 import ctypes as C
+import os
 from dataclasses import dataclass
 
 import numpy as np
@@ -111,6 +112,16 @@ class PoolGeometry:
         return self.layers * self.planes * self.num_blocks * self.run_bytes
 
 
+def hw_queues() -> int:
+    """Hardware queues per process HIP creates (GPU_MAX_HW_QUEUES when it
+    starts; its default is 4)."""
+    try:
+        n = int(os.environ.get("GPU_MAX_HW_QUEUES", "4"))
+    except ValueError:
+        return 4
+    return n if n > 0 else 4
+
+
 def _u32_dev(a: np.ndarray, device) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(a, np.uint32).view(np.int32).copy()).to(device)
 
@@ -120,7 +131,12 @@ class TierPool:
     host arena for the CPU tier, and a libmori context."""
 
     def __init__(self, geom, tbl_off, tbl, tier, free_map, arena_bytes: int, max_programs: int | None = None,
-                 staging_bytes: int = 0, device: str = "cuda", pool: torch.Tensor | None = None):
+                 staging_bytes: int = 0, device: str = "cuda", pool: torch.Tensor | None = None,
+                 copy_streams: bool | None = None):
+        """copy_streams: let the context own a copy stream per direction
+        (MORI_CREATE_COPY_STREAMS), which needs 8 hardware queues in the
+        process; None: decided from GPU_MAX_HW_QUEUES as this process set it
+        before HIP started."""
         self.geom = PoolGeometry(geom.layers, geom.planes, geom.block_tokens, geom.row_bytes, geom.num_blocks)
         self.device = torch.device(device)
         self.P = int(tier.size)
@@ -139,7 +155,10 @@ class TierPool:
         self.host_addr = np.zeros(max(self.P, 1), np.uint64)
         self._pool_desc = M.mori_pool(self.geom.layers, self.geom.planes, self.geom.block_tokens,
                                       self.geom.row_bytes, self.geom.num_blocks, self.pool.data_ptr())
-        rc, self.ctx = M.mori_create(self._pool_desc, max_programs or max(self.P, 1), staging_bytes)
+        if copy_streams is None:
+            copy_streams = hw_queues() >= 8
+        rc, self.ctx = M.mori_create(self._pool_desc, max_programs or max(self.P, 1), staging_bytes,
+                                     M.MORI_CREATE_COPY_STREAMS if copy_streams else 0)
         check(rc, "mori_create")
         check(M.mori_register(self.ctx, self.arena.ptr, self.arena.nbytes), "mori_register(arena)")
         self._keep = []

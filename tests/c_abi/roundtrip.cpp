@@ -142,7 +142,10 @@ int main(int argc, char** argv) {
   HIP_OK(hipStreamCreateWithFlags(&s_in, hipStreamNonBlocking));
   mori_pool mp{L, C, T, ROW, NB, d_pool};
   mori_ctx* ctx = nullptr;
-  MORI_OK_(mori_create(&mp, P, 16 * block, &ctx));  // small staging: many chunks per direction
+  // copy streams of its own only when this process has the hardware queues for them
+  const char* hwq = std::getenv("GPU_MAX_HW_QUEUES");
+  const uint32_t cflags = hwq && std::atoi(hwq) >= 8 ? MORI_CREATE_COPY_STREAMS : 0u;
+  MORI_OK_(mori_create(&mp, P, 16 * block, cflags, &ctx));  // small staging: many chunks per direction
   void* arena = nullptr;
   MORI_OK_(mori_host_alloc(ext[P] + 256, &arena));
   MORI_OK_(mori_register(ctx, arena, ext[P] + 256));

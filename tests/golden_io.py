@@ -57,6 +57,8 @@ def plan_cases():
         d["tables"] = _tables(kv["tables"])
         d["new_tables"] = _tables(kv["new_tables"])
         d["free"] = [int(x) for x in kv["free"].split()]
+        d["status"] = [STATUS[x] for x in kv["status"].split()] if "status" in kv else None
+        d["flags"] = kv.get("flags", "").split()
         d["new_free"] = [int(x) for x in kv["new_free"].split()]
         d["idleness"] = [float(x) for x in kv["idleness"].split()]
         d["summary"] = {k: int(v) for k, v in (t.split("=") for t in kv["summary"].split())}

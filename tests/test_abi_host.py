@@ -53,7 +53,26 @@ def test_create_rejects_bad_pools_on_host(M):
     for mp in (0, M.MORI_MAX_PROGRAMS + 1):
         rc, _ = M.mori_create(M.mori_pool(**ok), mp)
         assert rc == M.MORI_EINVAL
-    assert M.lib().mori_create(None, 8, 0, C.byref(C.c_void_p())) == M.MORI_EINVAL
+    assert M.lib().mori_create(None, 8, 0, 0, C.byref(C.c_void_p())) == M.MORI_EINVAL
+
+
+def test_create_flags_checked_on_host(M):
+    """The copy-stream choice is the caller's explicit flag: any other bit is
+    rejected before the HIP runtime is touched."""
+    ok = dict(layers=2, planes=2, block_tokens=16, row_bytes=512, num_blocks=8, base=0x100000)
+    for flags in (2, 4, 0x80000000, M.MORI_CREATE_COPY_STREAMS | 2):
+        rc, ctx = M.mori_create(M.mori_pool(**ok), 8, 0, flags)
+        assert rc == M.MORI_EINVAL and not ctx.value, flags
+
+
+def test_tierpool_copy_stream_choice(monkeypatch):
+    from paper_2606_00866_amd import tiering
+
+    for env, want in (("8", 8), ("32", 32), ("4", 4), ("", 4), ("x", 4), ("0", 4)):
+        monkeypatch.setenv("GPU_MAX_HW_QUEUES", env)
+        assert tiering.hw_queues() == want
+    monkeypatch.delenv("GPU_MAX_HW_QUEUES")
+    assert tiering.hw_queues() == 4
 
 
 def test_null_context_calls(M):

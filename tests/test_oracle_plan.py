@@ -24,9 +24,11 @@ def test_worked_examples(orc, name):
     c = plan_cases()[name]
     geom = Geometry(num_blocks=c["num_blocks"], **ONE)
     off, tbl, tier, free = _state_from_case(c)
-    res = orc.rebalance(geom, iota=np.array(c["idleness"], np.float32), tbl_off=off, tbl=tbl, tier=tier,
-                        free_map=free, gpu_budget=c["gpu_budget"], cpu_budget=c["cpu_budget"],
-                        flags=orc.F_IDLENESS_GIVEN)
+    flags = orc.F_IDLENESS_GIVEN | (orc.F_INCREMENTAL if "incremental" in c["flags"] else 0)
+    status = None if c["status"] is None else np.array(c["status"], np.uint8)
+    res = orc.rebalance(geom, iota=np.array(c["idleness"], np.float32), status=status, tbl_off=off, tbl=tbl,
+                        tier=tier, free_map=free, gpu_budget=c["gpu_budget"], cpu_budget=c["cpu_budget"],
+                        flags=flags)
     assert res.rc == orc.OK
     assert tier.tolist() == c["new_tier"]
     assert tbl.tolist() == [x for grp in c["new_tables"] for x in grp]
@@ -35,7 +37,9 @@ def test_worked_examples(orc, name):
         assert res.summary[k] == v, k
 
 
-def _check_invariants(orc, inst, res, tbl0, tier0, free0, tbl, tier, free, budgets):
+def _check_invariants(orc, inst, res, tbl0, tier0, free0, tbl, tier, free, budgets, running=None):
+    """running[p]: program p may still be running an inference step (Sec. 4.3.1
+    lazy demotion), so pages it leaves become free only after its step."""
     P, NB = inst.P, inst.geom.num_blocks
     off = inst.tbl_off
     nblk = inst.nblk.astype(np.int64)
@@ -59,13 +63,18 @@ def _check_invariants(orc, inst, res, tbl0, tier0, free0, tbl, tier, free, budge
     # allocation: pages handed out in the order free-before ++ dropped ++ swapped out, each ascending
     f0 = np.flatnonzero(free0)
 
-    def pages_of(leaving_to):
-        return np.sort(np.concatenate([tbl0[off[p]:off[p + 1]] for p in range(P)
-                                       if tier0[p] == 0 and tier[p] in leaving_to] + [np.zeros(0, np.uint32)]))
+    if running is None:
+        running = np.zeros(P, bool)
 
-    dropped = pages_of((2,))      # nothing reads them
-    swapped = pages_of((1, 3))    # free once the swap-out has read them
-    avail = np.concatenate([f0, dropped, swapped]).astype(np.int64)
+    def pages_of(keep):
+        return np.sort(np.concatenate([tbl0[off[p]:off[p + 1]] for p in range(P)
+                                       if tier0[p] == 0 and tier[p] != 0 and keep(p)] + [np.zeros(0, np.uint32)]))
+
+    # nothing reads these: dropped to Waiting and idle
+    dropped = pages_of(lambda p: tier[p] == 2 and not running[p])
+    # free only later: swapped out (after the swap-out read them) or dropped while running
+    later = pages_of(lambda p: tier[p] in (1, 3) or running[p])
+    avail = np.concatenate([f0, dropped, later]).astype(np.int64)
     assert res.summary["pages_dropped"] == dropped.size
     incoming = [p for p in res.order if tier0[p] == 1 and tier[p] == 0] + \
                [p for p in res.order if tier0[p] == 2 and tier[p] == 0]
@@ -98,7 +107,8 @@ def test_random_instances_invariants(orc, seed):
     assert res.rc == orc.OK
     if flags == orc.F_SKIP_FIT:
         return _check_invariants_skip(inst, tbl, tier, free, (bg, bc))
-    _check_invariants(orc, inst, res, tbl0, tier0, free0, tbl, tier, free, (bg, bc))
+    running = inst.status != orc.ST_ACTING if flags == orc.F_STATUS_KEY else None
+    _check_invariants(orc, inst, res, tbl0, tier0, free0, tbl, tier, free, (bg, bc), running)
 
 
 def _check_invariants_skip(inst, tbl, tier, free, budgets):
