@@ -5,14 +5,15 @@ Full-size Llama-3-8B, Llama-3-70B and MLA pools (136-155 GiB of HBM) and one
 rank's share of the Llama-3-70B programs under tensor parallelism of 2 (the
 same programs with 1 KiB rows and 16 KiB runs, 76 GiB): three
 boundary-policy steps, one incremental-policy step and one three-tier (SSD)
-step.  The oracle replays every step's placement and the per-step summaries,
-final block tables, tiers and free map must match exactly; every resident
-run's tag is checked and sampled runs are compared byte for byte with their
-content-addressed value.
+step.  The oracle replays every step's placement; after every step the
+summary, block tables, tiers and free map must match it exactly, and every
+byte of every resident run -- each page of each GPU-resident program and each
+host buffer of the CPU and SSD tiers -- must equal its content-addressed
+value (regenerated and compared on the device).
 
 Churn (1024 programs, 100 steps, GPU budget swinging 45-65%, 10% of programs
 flipping phase per step), scaled to fit one GPU and the pinned-memory ceiling:
-placement and summary compared with the oracle after every step.
+the same checks after every step, in both copy modes.
 """
 import numpy as np
 import pytest
@@ -22,8 +23,8 @@ from gpu_helpers import log
 from oracle import oracle
 from paper_2606_00866_amd import mori as M
 from paper_2606_00866_amd.tiering import TierPool
-from workload import (CHURN, LLAMA3_70B, LLAMA3_70B_TP2, LLAMA3_8B, MLA, budget_bytes, churn_steps, fill_pool_torch,
-                      make_bank, make_instance, program_content_torch, run_content, run_tag)
+from workload import (CHURN, LLAMA3_70B, LLAMA3_70B_TP2, LLAMA3_8B, MLA, budget_bytes, check_tier_bytes, churn_steps,
+                      fill_pool_torch, make_bank, make_instance, program_content_torch)
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 GIB = 1 << 30
@@ -50,6 +51,7 @@ class Harness:
         self.valid = np.ones(inst.P, bool)
         self.s_out, self.s_in = torch.cuda.Stream(), torch.cuda.Stream()
         self.steps = 0
+        self.bytes_checked = 0
 
     def close(self):
         torch.cuda.synchronize()
@@ -76,6 +78,7 @@ class Harness:
         tbl, tier, free = self.tp.state()
         assert (tbl == self.tbl).all() and (tier == self.tier).all() and (free == self.free).all(), self.steps
         self.prefill(res.category)
+        self.check_all_bytes()
         self.steps += 1
         return plan
 
@@ -99,42 +102,14 @@ class Harness:
             program_content_torch(inst, self.bank_dev, int(p), out=dst)  # one copy into the pinned tier
         torch.cuda.synchronize()
 
-    def check_tags(self):
-        """The tag of every run of every resident program sits where the tables
-        (GPU) or the program's host buffer (CPU) say."""
-        inst, g = self.inst, self.g
-        planes = self.tp.pool.view(torch.int32).view(g.nplanes, g.num_blocks, g.run_bytes // 4)
-        for p in range(inst.P):
-            n = int(inst.nblk[p])
-            if n == 0 or self.tier[p] == 2:
-                continue
-            q = np.repeat(np.arange(g.nplanes), n)
-            i = np.tile(np.arange(n), g.nplanes)
-            want = run_tag(np.full(q.size, p, np.int64), i.astype(np.int64), q.astype(np.int64)).astype(np.uint32)
-            if self.tier[p] == 0:
-                pages = torch.from_numpy(self.tbl[inst.tbl_off[p]:inst.tbl_off[p + 1]].astype(np.int64)).cuda()
-                got = planes[:, pages, 0].reshape(-1).cpu().numpy().view(np.uint32)
-            else:
-                got = self.tp.host_view(p).view(np.uint32).reshape(g.nplanes * n, g.run_bytes // 4)[:, 0]
-            assert (got == want).all(), ("tag", p, int(self.tier[p]))
-
-    def check_bytes(self, per_program=4, seed=0):
-        inst, g = self.inst, self.g
-        rng = np.random.default_rng(seed)
-        planes = self.tp.pool.view(g.nplanes, g.num_blocks, g.run_bytes)
-        n_checked = 0
-        for p in np.flatnonzero((self.tier != 2) & (inst.nblk > 0)):
-            n = int(inst.nblk[p])
-            for _ in range(per_program):
-                i, q = int(rng.integers(0, n)), int(rng.integers(0, g.nplanes))
-                expect = run_content(self.bank, g.run_bytes, p, i, q)[0]
-                if self.tier[p] == 0:
-                    got = planes[q, int(self.tbl[inst.tbl_off[p] + i])].cpu().numpy()
-                else:
-                    got = self.tp.host_view(int(p))[(q * n + i) * g.run_bytes:(q * n + i + 1) * g.run_bytes]
-                assert np.array_equal(got, expect), ("bytes", int(p), i, q)
-                n_checked += 1
-        return n_checked
+    def check_all_bytes(self):
+        """Every resident run equals its content-addressed value: all pages of
+        every GPU-resident program (through the tables) and every CPU/SSD host
+        buffer, compared on the device."""
+        r = check_tier_bytes(self.tp.pool, self.g, self.inst.tbl_off, self.tbl, self.tier, self.bank_dev,
+                             self.tp.host_view)
+        assert r["ok"], (self.steps, r)
+        self.bytes_checked += r["bytes"]
 
 
 @pytest.mark.parametrize("cfg", [LLAMA3_8B, LLAMA3_70B, LLAMA3_70B_TP2, MLA], ids=lambda c: c.name)
@@ -170,8 +145,7 @@ def test_full_size_workload(cfg):
         plan = h.step(inst.window, bg, bc, flags=oracle.F_SSD_TIER, ssd=8 * GIB)
         log(f"  SSD step: m_ssd {plan.m_ssd} out {plan.n_out} in {plan.n_in}")
         assert plan.m_ssd > 0
-        h.check_tags()
-        log(f"  sampled runs checked: {h.check_bytes()}")
+        log(f"  bytes compared over {h.steps} steps: {h.bytes_checked / GIB:.1f} GiB")
     finally:
         h.close()
 
@@ -195,10 +169,8 @@ def test_churn_scaled():
             recycled_steps += plan.pages_recycled > 0
             if t % 20 == 0:
                 log(f"  step {t}: pct {pct:.1f} out {plan.bytes_out / GIB:.2f} in {plan.bytes_in / GIB:.2f} GiB "
-                    f"recycled {plan.pages_recycled}")
-                h.check_bytes(per_program=1, seed=t)
+                    f"recycled {plan.pages_recycled}, {h.bytes_checked / GIB:.1f} GiB compared so far")
         assert moved > 0
         assert recycled_steps > 0  # swap-ins onto pages released by the same step's swap-out
-        h.check_tags()
     finally:
         h.close()

@@ -194,6 +194,30 @@ def churn_steps(cfg: KVConfig, busy0: np.ndarray, steps: int | None = None):
         yield t, pct, busy.copy(), draw_windows(rng, busy)
 
 
+# Window sets of the rotation schedule: (reasoning, tool-call) seconds drawn
+# uniformly per cycle.  The three sets never interleave in idleness: over k
+# cycles the busy set's tool time is at most 0.3k s against at least 1.5k s of
+# reasoning (idleness below 0.3 / 1.8 = 0.17), the middle set's lies in
+# [2k, 4k] against [1.5k, 2.5k] (idleness in [2 / 4.5, 4 / 5.5] = [0.44, 0.73])
+# and the idle set's in [40k, 80k] (idleness above 40 / 42.5 = 0.94).
+ROTATION_SETS = ((1.5, 2.5, 0.0, 0.3), (1.5, 2.5, 2.0, 4.0), (1.5, 2.5, 40.0, 80.0))
+
+
+def rotation_windows(seed: int, P: int, steps: int, k: int = WINDOW_K) -> np.ndarray:
+    """float32 [steps][3][P][k][2] windows, redrawn every step: set 0 busy
+    (tool calls that have just ended), set 1 middle, set 2 idle (long tool
+    calls).  A schedule that gives each program the set of its current tier
+    (CPU tier busy, GPU tier middle, Waiting idle) makes the CPU tier the
+    busiest every step, so every step moves KV both ways; within a set the
+    drawn windows order the programs."""
+    rng = _streams(seed, 7)[6]
+    out = np.empty((steps, 3, P, k, 2), np.float32)
+    for j, (r_lo, r_hi, a_lo, a_hi) in enumerate(ROTATION_SETS):
+        out[:, j, :, :, 0] = rng.uniform(r_lo, r_hi, size=(steps, P, k))
+        out[:, j, :, :, 1] = rng.uniform(a_lo, a_hi, size=(steps, P, k))
+    return out
+
+
 # --------------------------------------------------------------------------
 # random small instances (parity and property tests)
 # --------------------------------------------------------------------------
@@ -347,6 +371,20 @@ def fill_pool_torch(pool, inst: Instance, bank_dev, owner_p=None, owner_i=None, 
             tags = run_tag(pp, ii, q)
             vals.view(torch.int32)[:, 0] = torch.where(tags >= 2**31, tags - 2**32, tags).to(torch.int32)
             dst[pages] = vals
+
+
+def runs_torch(bank_dev, run_bytes: int, p, i, q):
+    """Expected bytes of runs (p, i, q), generated on the device: p, i, q are
+    int64 tensors of equal length (or Python ints for q) on bank_dev's device;
+    returns int16 [n][run_bytes / 2]."""
+    import torch
+
+    e = run_bytes // 2
+    win = torch.as_strided(bank_dev, (BANK, e), (1, 1))
+    vals = torch.index_select(win, 0, run_offset(p, i, q))
+    tags = run_tag(p, i, q)
+    vals.view(torch.int32)[:, 0] = torch.where(tags >= 2**31, tags - 2**32, tags).to(torch.int32)
+    return vals
 
 
 def program_content_torch(inst: Instance, bank_dev, p: int, out=None):
