@@ -364,6 +364,22 @@ int mori_evict_order(const mori_blocks* blocks, uint32_t tier, uint64_t need_byt
                      uint64_t workspace_bytes, uint32_t* order, uint64_t* prefix, uint32_t* result,
                      void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops that forbid allocation): mori_evict_order with the
+ * workspace in a device array the library holds on each GPU for the life of
+ * the process, instead of a caller buffer.  Same result for the same input;
+ * at most MORI_EVICT_NOALLOC_MAX_BLOCKS blocks (ENOSPC above; the array is
+ * about 19.5 MiB per GPU).  Nothing is allocated: the array's device address
+ * is looked up on the first call on each GPU (call it once before a capture
+ * starts), and each call enqueues kernels only, which clear what must start
+ * at zero.  Every call on one GPU uses the same array: calls whose work
+ * overlaps on one GPU (other streams, other host threads) race and give
+ * wrong results, so the caller serialises them, e.g. on one stream.
+ * EINVAL: null pointers, bad tier; EHIP: the address lookup failed. */
+#define MORI_EVICT_NOALLOC_MAX_BLOCKS 524288u /* 2^19 */
+int mori_evict_order_noalloc(const mori_blocks* blocks, uint32_t tier, uint64_t need_bytes, uint32_t* order,
+                             uint64_t* prefix, uint32_t* result, void* stream);
+
 /* ---- kernel timing ------------------------------------------------------ */
 /* With profiling on, every gather/scatter kernel launch of the swaps is
  * bracketed by timing events recorded on the stream it is launched on (up to

@@ -52,15 +52,12 @@
 namespace mori {
 namespace {
 
-constexpr int ET = 256;                 // threads per tile workgroup
+constexpr int ET = EVICT_WG;            // threads per tile workgroup
 constexpr int ENW = ET / 64;            // waves per tile workgroup
-// Keys per thread (tile = 256 x that): measured on MI355X with the bench's
-// block metadata, 4 is fastest up to ~2^19 blocks (more workgroups for a
-// latency-bound sort), 8 above (fewer tiles to scan per digit).
-constexpr uint32_t SMALL_SORT = 1u << 19;
-inline int keys_per_thread(uint32_t N) { return N <= SMALL_SORT ? 4 : 8; }
+// Keys per thread (tile = 256 x that), measured with the bench's block metadata.
+inline int keys_per_thread(uint32_t N) { return evict_keys_per_thread(N); }
 constexpr uint64_t TIME_LIMIT = 1ull << 62;
-constexpr uint32_t KEY_WG_MAX = 128;     // workgroups of the keys kernel at most (one digit-count set each)
+constexpr uint32_t KEY_WG_MAX = EVICT_KEY_WG_MAX;  // workgroups of the keys kernel at most (one digit-count set each)
 // Keys per thread whose loads the keys kernel issues together: 4 for the
 // look-back passes, 8 above (measured: 8 and 16 are 3 and 11 us slower at
 // 69 938 blocks, 8 is 2.5 us faster at 2^20).
@@ -722,14 +719,6 @@ void launch_tiles(const EvictArgs& a, hipStream_t s) {
 }
 
 }  // namespace
-
-uint64_t evict_workspace_bytes(uint32_t N) {
-  const uint64_t tile = (uint64_t)ET * keys_per_thread(N);
-  const uint64_t ntiles = ((uint64_t)N + tile - 1) / tile;
-  auto up = [](uint64_t b) { return (b + 255) & ~255ull; };
-  return 2 * up(8ull * N) + 2 * up(4ull * N) + up(4ull * 256 * ntiles) + up(4 * 256) + 2 * up(8ull * 256 * ntiles) +
-         up(4ull * KEY_WG_MAX * 8 * 256) + up(4 * 8 * 256) + up(4 * 8) + up(8ull * ntiles) + up(8ull * N) + up(8 * 4);
-}
 
 hipError_t launch_evict(uint32_t N, const uint8_t* type, const uint64_t* last_access, const uint32_t* size,
                         uint64_t unit_bytes, uint32_t tier, uint64_t need, void* workspace, uint32_t* order,

@@ -110,13 +110,34 @@ struct TranslateArgs {
   uint32_t* swap_err;       // [2]: this direction's word is swap_err[dir_in]
 };
 
+// Typed eviction order: workgroup size, keys per thread (measured on MI355X:
+// 4 is fastest up to ~2^19 blocks, more workgroups for a latency-bound sort;
+// 8 above, fewer tiles to scan per digit), keys-kernel workgroups at most.
+constexpr int EVICT_WG = 256;
+constexpr uint32_t EVICT_SMALL_SORT = 1u << 19;
+constexpr uint32_t EVICT_KEY_WG_MAX = 128;
+constexpr int evict_keys_per_thread(uint32_t N) { return N <= EVICT_SMALL_SORT ? 4 : 8; }
+
+// Device workspace of the eviction order for N blocks, in the order
+// launch_evict lays it out (each piece 256-B aligned): two key and two value
+// buffers, the tile histogram, digit totals, two look-back status arrays,
+// per-workgroup digit counts, their totals, tile counters, tile sums, a
+// prefix buffer and a few words of results.
+constexpr uint64_t evict_workspace_bytes(uint32_t N) {
+  const uint64_t tile = (uint64_t)EVICT_WG * evict_keys_per_thread(N);
+  const uint64_t ntiles = ((uint64_t)N + tile - 1) / tile;
+  auto up = [](uint64_t b) { return (b + 255) & ~255ull; };
+  return 2 * up(8ull * N) + 2 * up(4ull * N) + up(4ull * 256 * ntiles) + up(4 * 256) + 2 * up(8ull * 256 * ntiles) +
+         up(4ull * EVICT_KEY_WG_MAX * 8 * 256) + up(4 * 8 * 256) + up(4 * 8) + up(8ull * ntiles) + up(8ull * N) +
+         up(8 * 4);
+}
+
 // launchers (return the launch error)
 hipError_t launch_rank(const PlanArgs& a, hipStream_t s);
 hipError_t launch_pages(const PlanArgs& a, hipStream_t s);
 hipError_t launch_translate(const TranslateArgs& a, hipStream_t s);
 hipError_t launch_swap_out(const SwapArgs& a, uint32_t grid, hipStream_t s);
 hipError_t launch_swap_in(const SwapArgs& a, uint32_t grid, hipStream_t s);
-uint64_t evict_workspace_bytes(uint32_t N);
 hipError_t launch_evict(uint32_t N, const uint8_t* type, const uint64_t* last_access, const uint32_t* size,
                         uint64_t unit_bytes, uint32_t tier, uint64_t need, void* workspace, uint32_t* order,
                         uint64_t* prefix, uint32_t* result, hipStream_t s);

@@ -29,13 +29,14 @@ MORI_CREATE_COPY_STREAMS = 1
  MORI_CAT_ADMIT_CPU, MORI_CAT_CPU_SSD, MORI_CAT_SSD_CPU, MORI_CAT_DROP_SSD, MORI_CAT_ADMIT_SSD) = range(11)
 MORI_MAX_PROGRAMS, MORI_MAX_WINDOW, MORI_MAX_RANGES, MORI_MAX_REPLICAS = 4096, 64, 64, 1024
 MORI_ADMIT_BEST_FIT = 1
+MORI_EVICT_NOALLOC_MAX_BLOCKS = 1 << 19
 MORI_Q_LAST_HIP_ERROR, MORI_Q_DEVICE_ERROR, MORI_Q_LAST_MODE = 1, 2, 3
 MORI_Q_PLAN_EVENT, MORI_Q_OUT_EVENT, MORI_Q_IN_EVENT = 4, 5, 6
 
 EXPORTS = ("mori_create", "mori_destroy", "mori_register", "mori_host_alloc", "mori_host_free",
            "mori_rank_partition", "mori_plan_wait", "mori_kv_swap_out", "mori_kv_swap_in", "mori_query",
            "mori_strerror", "mori_profile", "mori_profile_read", "mori_evict_workspace", "mori_evict_order",
-           "mori_replica_admit")
+           "mori_replica_admit", "mori_evict_order_noalloc")
 
 
 class mori_pool(C.Structure):
@@ -98,6 +99,7 @@ def lib():
         L.mori_evict_workspace.argtypes = [U32, C.POINTER(U64)]
         L.mori_evict_order.argtypes = [C.POINTER(mori_blocks), U32, U64, V, U64, V, V, V, V]
         L.mori_replica_admit.argtypes = [U32, V, V, V, U32, V, U32, V, V]
+        L.mori_evict_order_noalloc.argtypes = [C.POINTER(mori_blocks), U32, U64, V, V, V, V]
         L.mori_strerror.restype = C.c_char_p
         for name in EXPORTS:
             if name != "mori_strerror":
@@ -181,6 +183,12 @@ def mori_evict_order(blocks: mori_blocks, tier: int, need_bytes: int, workspace:
     """order / prefix / result / workspace: device addresses (prefix may be 0)."""
     return lib().mori_evict_order(C.byref(blocks), tier, need_bytes, workspace, workspace_bytes, order,
                                   prefix or None, result, stream)
+
+
+def mori_evict_order_noalloc(blocks: mori_blocks, tier: int, need_bytes: int, order: int, prefix: int,
+                             result: int, stream: int = 0) -> int:
+    """mori_evict_order without a workspace (the library's device array is used)."""
+    return lib().mori_evict_order_noalloc(C.byref(blocks), tier, need_bytes, order, prefix or None, result, stream)
 
 
 def mori_replica_admit(bytes_, idleness, status, room, flags: int = 0):
