@@ -3,16 +3,23 @@
 
 One step = one whole rebalance: Eq. 1 idleness -> ranking -> GPU/CPU/Waiting
 boundaries -> sticky diff and page allocation -> swap-out (GPU -> pinned host)
-concurrently with swap-in (pinned host -> GPU) on two streams.  Steps
-alternate between the drawn idleness windows and the reversed windows (every
-program's reasoning and tool-call times swapped), so each timed step moves
-programs in both directions.
+concurrently with swap-in (pinned host -> GPU) on two streams.
+
+The headline workload is the compressed-latent (MLA-style) one, the largest
+that fits one GPU (256 programs, a 155 GiB pool, 72 KiB runs).  Its schedule
+rotates the tiers through idleness windows: every step each program gets
+windows of its current tier's set (CPU tier busy, GPU tier middle, Waiting
+idle, redrawn per step), so the kernel computes Eq. 1 on the device every
+step and the CPU tier comes back while as many bytes leave the GPU.  The
+Llama-3-8B workload follows as a second leg (drawn and reversed windows,
+alternating).
 
 value = KV migration GB/s = (bytes swapped out + bytes swapped in) / step wall
 time, with the pool, tables and windows already resident in HBM and the CPU
 tier already in pinned host memory when the timed region starts.  The
-host-link peak (pinned hipMemcpyAsync, D2H / H2D / both at once) and the HBM
-copy peak are measured in the same run.  The roofline object is for the
+host-link peaks (pinned hipMemcpyAsync: D2H, H2D, and both directions at
+once as chunk streams, rate over the window where both run) and the HBM copy
+peak are measured in the same run.  The roofline object is for the
 gather/scatter kernel (HBM-bound), timed per launch with events on its stream.
 """
 from __future__ import annotations
@@ -51,12 +58,16 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=6)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="llama3_8b")
+    ap.add_argument("--workload", default="mla")
     ap.add_argument("--scale", type=float, default=None,
                     help="context scale (churn: default 0.32, a ~120 GiB pool; others: 1)")
-    ap.add_argument("--schedule", default="reverse", choices=["reverse", "rotate"],
-                    help="reverse: steps alternate drawn and reversed windows; rotate: each step the CPU-tier "
-                         "programs become the busiest (idleness given), so both directions move every step")
+    ap.add_argument("--schedule", default=None, choices=["reverse", "rotate"],
+                    help="reverse: steps alternate drawn and reversed windows; rotate: each step every program "
+                         "gets windows of its tier's set (CPU busy, GPU middle, Waiting idle), so both directions "
+                         "move every step (default: rotate for mla, reverse otherwise)")
+    ap.add_argument("--extra", default="llama3_8b",
+                    help="comma-separated workloads timed after the headline one ('' for none)")
+    ap.add_argument("--extra-steps", type=int, default=4)
     ap.add_argument("--mode", default="auto", choices=["auto", "kernel", "ce"])
     ap.add_argument("--arena-gib", type=float, default=60.0, help="pinned CPU-tier arena")
     ap.add_argument("--cpu-gib", type=float, default=28.0, help="CPU-tier budget")
@@ -73,7 +84,26 @@ def parse():
 # --------------------------------------------------------------------------
 # CPU baseline: the oracle, as it stands, on a bounded sample of the workload
 # --------------------------------------------------------------------------
-def cpu_baseline(cfg, cpu_frac: float, seconds: float, evict_sizes=(), plan_cases=()):
+# tier -> rotation window set: GPU middle, CPU busy, Waiting (and SSD) idle
+ROT_SET_OF_TIER = (1, 0, 2, 2)
+
+
+def schedule_windows(np, inst, schedule: str, steps: int):
+    """Host windows of step t given the tiers before it: 'reverse' alternates
+    the drawn and the reversed windows (every program's reasoning and tool
+    times swapped); 'rotate' gives each program a window of its tier's set."""
+    from workload import rotation_windows
+
+    if schedule == "rotate":
+        rot = rotation_windows(inst.seed, inst.P, steps)
+        sel = np.array(ROT_SET_OF_TIER)
+        ar = np.arange(inst.P)
+        return lambda t, tier: np.ascontiguousarray(rot[t % steps][sel[tier], ar])
+    wins = (np.ascontiguousarray(inst.window), inst.window[:, :, ::-1].copy())
+    return lambda t, tier: wins[t % 2]
+
+
+def cpu_baseline(cfg, schedule: str, cpu_frac: float, seconds: float, evict_sizes=(), plan_cases=()):
     import numpy as np
 
     from oracle import oracle
@@ -88,12 +118,13 @@ def cpu_baseline(cfg, cpu_frac: float, seconds: float, evict_sizes=(), plan_case
     tbl, tier, free = inst.copy_state()
     bg = budget_bytes(inst.total_bytes, cfg.gpu_pct)
     bc = int(inst.total_bytes * cpu_frac)
-    wins = (inst.window, inst.window[:, :, ::-1].copy())
+    window_of = schedule_windows(np, inst, schedule, 256)
     moved, spent, steps = 0, 0.0, 0
     t = 0
     while True:
+        w = window_of(t, tier)
         t0 = time.perf_counter()
-        res = oracle.rebalance(g, window=wins[t % 2], tbl_off=inst.tbl_off, tbl=tbl, tier=tier, free_map=free,
+        res = oracle.rebalance(g, window=w, tbl_off=inst.tbl_off, tbl=tbl, tier=tier, free_map=free,
                                gpu_budget=bg, cpu_budget=bc, pool=pool, host_bufs=bufs)
         dt = time.perf_counter() - t0
         assert res.rc == oracle.OK
@@ -106,8 +137,9 @@ def cpu_baseline(cfg, cpu_frac: float, seconds: float, evict_sizes=(), plan_case
             break
     out = {"value": round(moved / spent / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
            "sample": (f"{cfg.name} with contexts scaled by {scale:g} ({inst.P} programs, "
-                      f"{inst.total_bytes / GIB:.2f} GiB of KV, same GPU/CPU budget fractions), {steps} "
-                      f"bidirectional rebalances, memcpy per run between host buffers, single thread")}
+                      f"{inst.total_bytes / GIB:.2f} GiB of KV, same GPU/CPU budget fractions, {schedule} "
+                      f"schedule), {steps} bidirectional rebalances, memcpy per run between host buffers, "
+                      f"single thread")}
     # the same oracle on all of this process's cores: one thread per core, each
     # rebalancing its own copy of a smaller sample (the C oracle runs outside
     # the GIL and shares no state between calls)
@@ -119,7 +151,7 @@ def cpu_baseline(cfg, cpu_frac: float, seconds: float, evict_sizes=(), plan_case
     sbank = make_bank(cfg.seed, cfg.dtype, sg.run_bytes)
     sbg = budget_bytes(small.total_bytes, cfg.gpu_pct)
     sbc = int(small.total_bytes * cpu_frac)
-    swins = (small.window, small.window[:, :, ::-1].copy())
+    swindow_of = schedule_windows(np, small, schedule, 256)
     moved_t = [0] * threads
     stop = threading.Event()
 
@@ -133,7 +165,7 @@ def cpu_baseline(cfg, cpu_frac: float, seconds: float, evict_sizes=(), plan_case
             ready.wait(timeout=300)
             t = 0
             while not stop.is_set():
-                r = oracle.rebalance(sg, window=swins[t % 2], tbl_off=small.tbl_off, tbl=tbl_w, tier=tier_w,
+                r = oracle.rebalance(sg, window=swindow_of(t, tier_w), tbl_off=small.tbl_off, tbl=tbl_w, tier=tier_w,
                                      free_map=free_w, gpu_budget=sbg, cpu_budget=sbc, pool=pool_w, host_bufs=bufs_w)
                 if t >= 1 and not stop.is_set():
                     moved_t[w] += r.summary["bytes_out"] + r.summary["bytes_in"]
@@ -203,6 +235,20 @@ def cpu_baseline(cfg, cpu_frac: float, seconds: float, evict_sizes=(), plan_case
 # --------------------------------------------------------------------------
 # peaks measured in the same run
 # --------------------------------------------------------------------------
+def bytes_done_by(ends, w: float, chunk: int) -> float:
+    """Bytes a stream of equal chunks, started at time 0 and ending at the
+    given times, had moved by time w: the chunks ended by then, plus the
+    share of the one under way that its own span puts before w."""
+    prev = 0.0
+    for c, e in enumerate(ends):
+        if e > w:
+            return (c + (w - prev) / max(e - prev, 1e-12)) * chunk
+        prev = e
+    return float(len(ends) * chunk)
+
+
+# --------------------------------------------------------------------------
+# --------------------------------------------------------------------------
 def measure_peaks(torch, M, s1, s2):
     # the HIP runtime torch already loaded (a second copy of the runtime must never be loaded)
     hip = C.CDLL("libamdhip64.so.7", mode=os.RTLD_NOLOAD | os.RTLD_GLOBAL)
@@ -242,30 +288,41 @@ def measure_peaks(torch, M, s1, s2):
     t_h2d = timed(lambda: cp(dev_b.data_ptr(), h2, H2D, s1))
     t_bi = timed(lambda: (cp(h1, dev_a.data_ptr(), D2H, s1), cp(dev_b.data_ptr(), h2, H2D, s2)))
 
-    # Concurrent capacity: D2H and H2D started together, each timed to its own
-    # end.  The direction that ends first ran overlapped all along; the other
-    # one moved the rest of its bytes alone, at its one-direction rate, after
-    # that, so its overlapped rate follows; their sum is what both directions
-    # carry at once (the wall time of the pair undercounts it when they end at
-    # different times).
-    caps = []
-    for _ in range(5):
-        torch.cuda.synchronize()
-        e0 = torch.cuda.Event(enable_timing=True)
-        e_d, e_h = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(s1)
-        s2.wait_event(e0)
-        cp(h1, dev_a.data_ptr(), D2H, s1)
-        e_d.record(s1)
-        cp(dev_b.data_ptr(), h2, H2D, s2)
-        e_h.record(s2)
-        torch.cuda.synchronize()
-        td, th = e0.elapsed_time(e_d) / 1e3, e0.elapsed_time(e_h) / 1e3
-        (t_first, t_last, alone) = (td, th, n / t_h2d) if td <= th else (th, td, n / t_d2h)
-        r_first = n / t_first
-        r_last = max(0.0, n - alone * (t_last - t_first)) / t_first
-        caps.append(r_first + r_last)
-    cap = sorted(caps)[len(caps) // 2]
+    # Both directions at once, as streams of copies (D2H on s1, H2D on s2,
+    # started together, 16 GiB each way cycling over the 4 GiB buffers), each
+    # copy's end recorded by an event on its stream.  The rate is taken over
+    # the window in which both directions run: from the start to the end of
+    # the direction that finishes first, counting the bytes each direction
+    # completed inside it (the copy that straddles the window's end counted
+    # pro rata over its own span).  Two copy sizes (the swaps' copies range
+    # up to a 1 GiB staging half); the better median is the peak.
+    stream_bytes = 4 * n
+    steady = {}
+    for chunk in (256 << 20, 1 << 30):
+        nch = stream_bytes // chunk
+        per_buf = n // chunk
+        runs = []
+        for _ in range(5):
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            ev_d = [torch.cuda.Event(enable_timing=True) for _ in range(nch)]
+            ev_h = [torch.cuda.Event(enable_timing=True) for _ in range(nch)]
+            e0.record(s1)
+            s2.wait_event(e0)
+            for c in range(nch):
+                o = (c % per_buf) * chunk
+                assert hip.hipMemcpyAsync(h1 + o, dev_a.data_ptr() + o, chunk, D2H, C.c_void_p(s1.cuda_stream)) == 0
+                ev_d[c].record(s1)
+                assert hip.hipMemcpyAsync(dev_b.data_ptr() + o, h2 + o, chunk, H2D, C.c_void_p(s2.cuda_stream)) == 0
+                ev_h[c].record(s2)
+            torch.cuda.synchronize()
+            td = [e0.elapsed_time(e) / 1e3 for e in ev_d]
+            th = [e0.elapsed_time(e) / 1e3 for e in ev_h]
+            w = min(td[-1], th[-1])
+            bd, bh = bytes_done_by(td, w, chunk), bytes_done_by(th, w, chunk)
+            runs.append(((bd + bh) / w, bd / w, bh / w))
+        steady[chunk] = sorted(runs)[2]
+    best = max(steady, key=lambda k: steady[k][0])
     t_d2d = timed(lambda: cp(dev_b.data_ptr(), dev_a.data_ptr(), D2D, s1))
     torch.cuda.synchronize()
     M.mori_host_free(h1)
@@ -273,12 +330,15 @@ def measure_peaks(torch, M, s1, s2):
     del dev_a, dev_b
     torch.cuda.empty_cache()
     return {"d2h_GBps": round(n / t_d2h / 1e9, 2), "h2d_GBps": round(n / t_h2d / 1e9, 2),
-            "bidir_pair_GBps": round(2 * n / t_bi / 1e9, 2), "bidir_GBps": round(max(2 * n / t_bi, cap) / 1e9, 2),
+            "bidir_pair_GBps": round(2 * n / t_bi / 1e9, 2), "bidir_GBps": round(steady[best][0] / 1e9, 2),
+            "bidir_split_GBps": {"d2h": round(steady[best][1] / 1e9, 2), "h2d": round(steady[best][2] / 1e9, 2)},
+            "bidir_by_copy_GBps": {f"{k >> 20} MiB": round(v[0] / 1e9, 2) for k, v in steady.items()},
             "d2d_copy_GBps": round(2 * n / t_d2d / 1e9, 1),
-            "method": ("pinned hipMemcpyAsync, 4 GiB per direction, median of 5.  bidir_pair: D2H and H2D started "
-                       "together on two streams, 8 GiB over the time both took.  bidir: the larger of that and the "
-                       "concurrent capacity (overlapped rate of the direction that ended first plus the overlapped "
-                       "rate of the other, its tail after the first ended taken at its one-direction rate)")}
+            "method": ("pinned hipMemcpyAsync, 4 GiB per direction, median of 5.  bidir_pair: one D2H and one H2D "
+                       "copy started together on two streams, 8 GiB over the time both took.  bidir: D2H and H2D "
+                       "started together as streams of 16 GiB each in 256 MiB or 1 GiB copies with an event after "
+                       "each, bytes both directions completed while both ran over the time until the first of them "
+                       "finished, the better copy size (bidir_by_copy; bidir_split: each direction's share)")}
 
 
 def link_bound_s(out_bytes: int, in_bytes: int, peaks: dict) -> float:
@@ -458,29 +518,14 @@ def stored_traffic(workload: str, direction: int):
     return rec["gather" if direction == 0 else "scatter"]["traffic_bytes_per_launch"]
 
 
-def main() -> int:
-    args = parse()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print("bench.py runs on exactly one GPU: the KV migration path moves one GPU's pool to its own "
-              "host memory and has no multi-GPU form here (--gpus 1).", file=sys.stderr)
-        return 2
-
-    import numpy as np
-    import torch
-
-    # The two swap streams are the process's first streams: HIP maps streams to
-    # a small number of hardware queues (4 per process by default) and streams
-    # created later share queues, which serialises swap-out with swap-in.
-    s_out, s_in = torch.cuda.Stream(), torch.cuda.Stream()
-
-    from paper_2606_00866_amd import mori as M
+def run_workload(args, name, schedule, steps, warmup, s_out, s_in, peaks, torch, np, M):
+    """Times `steps` rebalances of one workload (after `warmup` untimed ones)
+    and checks the final state; the pool and the CPU tier are freed before it
+    returns."""
     from paper_2606_00866_amd.tiering import TierPool, check
-    from workload import CONFIGS, budget_bytes, churn_steps, fill_pool_torch, make_bank, make_instance, run_content
+    from workload import CONFIGS, budget_bytes, churn_steps, fill_pool_torch, make_bank, make_instance
 
-    cfg = CONFIGS[args.workload]
-    M.lib()
-    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    cfg = CONFIGS[name]
     churn = cfg.name == "churn"  # 1024 programs, nothing placed yet, budget swinging, phases flipping
     scale = args.scale if args.scale is not None else (0.32 if churn else 1.0)
     inst = make_instance(cfg, scale=scale, resident="wait" if churn else "gpu")
@@ -490,20 +535,9 @@ def main() -> int:
     bc = int(args.cpu_gib * GIB)
     # churn: step 0 places the first partition; step t >= 1 takes the t-th budget and windows
     churn_inputs = ([(budget_bytes(total, pct), w) for _, pct, _, w in
-                     churn_steps(cfg, inst.busy, steps=args.warmup + args.steps)] if churn else None)
+                     churn_steps(cfg, inst.busy, steps=warmup + steps)] if churn else None)
     log(f"workload {cfg.name}: P={inst.P} NB={g.num_blocks} block={g.block_bytes} B total={total / GIB:.2f} GiB "
-        f"gpu_budget={bg / GIB:.2f} GiB cpu_budget={bc / GIB:.2f} GiB")
-
-    evict_sizes = () if args.no_evict else (g.num_blocks, 1 << 20)
-    cases = () if args.no_plan else plan_cases(np, inst, bg, bc)
-    cpu = None
-    if not args.no_cpu_baseline:
-        t0 = time.perf_counter()
-        cpu = cpu_baseline(cfg, bc / total, args.cpu_seconds, evict_sizes, cases)
-        log(f"cpu baseline {cpu['value']} GB/s ({time.perf_counter() - t0:.1f} s)")
-
-    peaks = measure_peaks(torch, M, s_out, s_in)
-    log(f"peaks {peaks}")
+        f"gpu_budget={bg / GIB:.2f} GiB cpu_budget={bc / GIB:.2f} GiB schedule={schedule}")
 
     free_b, _ = torch.cuda.mem_get_info()
     need = g.pool_bytes + 2 * args.staging_mib * (1 << 20) + (2 << 30)
@@ -520,7 +554,13 @@ def main() -> int:
                   max_programs=inst.P, staging_bytes=args.staging_mib << 20, pool=pool)
     mode = {"auto": M.MORI_COPY_AUTO, "kernel": M.MORI_COPY_KERNEL, "ce": M.MORI_COPY_CE}[args.mode]
     wins = [torch.from_numpy(inst.window).cuda(), torch.from_numpy(inst.window[:, :, ::-1].copy()).cuda()]
-    rot_levels = torch.tensor([0.5, 0.1, 0.9], dtype=torch.float32, device="cuda")  # indexed by tier
+    if schedule == "rotate":
+        from workload import rotation_windows
+
+        # every step's three window sets, resident before the timed region
+        rot = torch.from_numpy(rotation_windows(cfg.seed, inst.P, warmup + steps)).cuda()
+        rot_sel = torch.tensor(ROT_SET_OF_TIER, dtype=torch.int64, device="cuda")
+        prog_ids = torch.arange(inst.P, device="cuda")
     if churn:
         churn_inputs = [(b, torch.from_numpy(np.ascontiguousarray(w)).cuda()) for b, w in churn_inputs]
     step_bg = [bg]  # the GPU budget of the last step
@@ -536,11 +576,10 @@ def main() -> int:
             bg_t, w_t = (bg, wins[0]) if t == 0 else churn_inputs[t - 1]
             step_bg[0] = bg_t
             check(tp.rank_partition(gpu_bytes=bg_t, cpu_bytes=bc, window=w_t, stream=s_out), "rank")
-        elif args.schedule == "rotate":  # CPU tier busiest, then GPU tier, Waiting last
+        elif schedule == "rotate":  # each program's window from its tier's set: Eq. 1 on the device
             with torch.cuda.stream(s_out):
-                iota = rot_levels[tp.tier.long()]
-            check(tp.rank_partition(gpu_bytes=bg, cpu_bytes=bc, idleness=iota, flags=M.MORI_F_IDLENESS_GIVEN,
-                                    stream=s_out), "rank")
+                w_t = rot[t][rot_sel[tp.tier.long()], prog_ids]
+            check(tp.rank_partition(gpu_bytes=bg, cpu_bytes=bc, window=w_t, stream=s_out), "rank")
         else:
             check(tp.rank_partition(gpu_bytes=bg, cpu_bytes=bc, window=wins[t % 2], stream=s_out), "rank")
         e_plan.record(s_out)
@@ -565,7 +604,7 @@ def main() -> int:
                                                    "pages_free_after", "pages_recycled", "bytes_out", "bytes_in")})
         return p
 
-    for t in range(args.warmup):
+    for t in range(warmup):
         p = one_step(t)
         log(f"warmup {t}: out {p.bytes_out / GIB:.2f} GiB in {p.bytes_in / GIB:.2f} GiB")
     _, last_mode = M.mori_query(tp.ctx, M.MORI_Q_LAST_MODE)
@@ -575,7 +614,7 @@ def main() -> int:
     torch.cuda.synchronize()
     moved = 0
     t_start = time.perf_counter()
-    for t in range(args.warmup, args.warmup + args.steps):
+    for t in range(warmup, warmup + steps):
         p = one_step(t, timed=True)
         moved += p.bytes_out + p.bytes_in
     torch.cuda.synchronize()
@@ -583,8 +622,8 @@ def main() -> int:
     prof = [M.mori_profile_read(tp.ctx, d) for d in (0, 1)]
     M.mori_profile(tp.ctx, False)
     value = moved / elapsed / 1e9
-    mix_bound_s = sum(link_bound_s(h["bytes_out"], h["bytes_in"], peaks) for h in history[-args.steps:])
-    log(f"timed {args.steps} steps: {moved / GIB:.2f} GiB in {elapsed:.3f} s -> {value:.2f} GB/s")
+    mix_bound_s = sum(link_bound_s(h["bytes_out"], h["bytes_in"], peaks) for h in history[-steps:])
+    log(f"timed {steps} steps: {moved / GIB:.2f} GiB in {elapsed:.3f} s -> {value:.2f} GB/s")
 
     # dominant kernel: the gather/scatter kernel of the direction on the step's
     # critical path (the direction whose work ends last)
@@ -595,13 +634,85 @@ def main() -> int:
                      "avg_launch_ms": round(ms / n, 4) if n else None,
                      "hbm_GBps": round(2 * by / (ms / 1e3) / 1e9, 1) if ms > 0 else None})
     crit = 0 if span[0] >= span[1] else 1
-    dom = kern[crit]
-    achieved = dom["hbm_GBps"] or 0.0
 
     verify = None
     if not args.no_verify:
-        verify = verify_sampled(inst, tp, bank, history, step_bg[0], bc, valid, np, run_content)
-        log(f"verify: {verify}")
+        t0 = time.perf_counter()
+        verify = verify_state(inst, tp, bank_dev, history, step_bg[0], bc, valid, np)
+        log(f"verify ({time.perf_counter() - t0:.1f} s): {verify}")
+    desc = (f"{cfg.name}: {inst.P} programs, {cfg.layers} layers x {cfg.planes} planes x {cfg.row_bytes} B rows "
+            f"({cfg.dtype}), {cfg.block_tokens}-token blocks ({g.run_bytes // 1024} KiB runs), {g.num_blocks} pages "
+            f"= {g.pool_bytes / GIB:.2f} GiB pool, GPU budget {cfg.gpu_pct}% of KV bytes, CPU tier "
+            f"{args.cpu_gib:g} GiB in a {args.arena_gib:g} GiB pinned arena; "
+            + (f"contexts scaled by {scale:g}, nothing placed before step 0, then per step the GPU budget swings "
+               f"{cfg.pct_swing[0]:g}+-{cfg.pct_swing[1]:g}% and {cfg.flip_frac:.0%} of programs flip phase"
+               if churn else
+               "steps alternate drawn / reversed idleness windows" if schedule == "reverse" else
+               "each step every program gets idleness windows of its tier's set (CPU tier busy, GPU tier middle, "
+               "Waiting idle; redrawn per step), Eq. 1 computed on the device"))
+    out = {"name": cfg.name, "value": value, "elapsed": elapsed, "moved": moved, "kern": kern, "crit": crit,
+           "span": span, "verify": verify, "desc": desc, "copy_mode": int(last_mode), "bg": bg, "bc": bc,
+           "mix_bound_s": mix_bound_s, "inst": inst}
+    tp.close()
+    del tp, pool, bank_dev, wins
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
+def main() -> int:
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on exactly one GPU: the KV migration path moves one GPU's pool to its own "
+              "host memory and has no multi-GPU form here (--gpus 1).", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    # The two swap streams are the process's first streams: HIP maps streams to
+    # a small number of hardware queues (4 per process by default) and streams
+    # created later share queues, which serialises swap-out with swap-in.
+    s_out, s_in = torch.cuda.Stream(), torch.cuda.Stream()
+
+    from paper_2606_00866_amd import mori as M
+    from workload import CONFIGS, budget_bytes, make_instance
+
+    cfg = CONFIGS[args.workload]
+    schedule = args.schedule or ("rotate" if cfg.name == "mla" else "reverse")
+    M.lib()
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    churn = cfg.name == "churn"
+    scale = args.scale if args.scale is not None else (0.32 if churn else 1.0)
+    inst0 = make_instance(cfg, scale=scale, resident="wait" if churn else "gpu")
+    bg0 = budget_bytes(inst0.total_bytes, cfg.gpu_pct)
+    bc = int(args.cpu_gib * GIB)
+    evict_sizes = () if args.no_evict else (inst0.geom.num_blocks, 1 << 20)
+    cases = () if args.no_plan else plan_cases(np, inst0, bg0, bc)
+    cpu = None
+    if not args.no_cpu_baseline:
+        t0 = time.perf_counter()
+        cpu = cpu_baseline(cfg, schedule, bc / inst0.total_bytes, args.cpu_seconds, evict_sizes, cases)
+        log(f"cpu baseline {cpu['value']} GB/s ({time.perf_counter() - t0:.1f} s)")
+
+    peaks = measure_peaks(torch, M, s_out, s_in)
+    log(f"peaks {peaks}")
+
+    head = run_workload(args, cfg.name, schedule, args.steps, args.warmup, s_out, s_in, peaks, torch, np, M)
+    others = {}
+    for name in [w for w in args.extra.split(",") if w and w != cfg.name]:
+        o = run_workload(args, name, "rotate" if name == "mla" else "reverse", args.extra_steps, args.warmup, s_out,
+                         s_in, peaks, torch, np, M)
+        k = o["kern"]
+        others[name] = {"value": round(o["value"], 3), "unit": "GB/s", "steps": args.extra_steps,
+                        "ms_per_step": round(o["elapsed"] / args.extra_steps * 1e3, 3),
+                        "bytes_per_step": int(o["moved"] / max(args.extra_steps, 1)), "workload": o["desc"],
+                        "frac_of_bidir_peak": round(o["value"] / peaks["bidir_GBps"], 4),
+                        "gather_hbm_GBps": k[0]["hbm_GBps"], "scatter_hbm_GBps": k[1]["hbm_GBps"],
+                        "gather_frac_of_hbm_peak": round((k[0]["hbm_GBps"] or 0) / HBM_PEAK_GBPS, 4),
+                        "scatter_frac_of_hbm_peak": round((k[1]["hbm_GBps"] or 0) / HBM_PEAK_GBPS, 4),
+                        "verify": o["verify"]}
 
     evict = None if args.no_evict else evict_leg(torch, np, M, evict_sizes)
     if evict:
@@ -613,6 +724,10 @@ def main() -> int:
     if replica:
         log(f"replica admission: {replica}")
 
+    kern, crit = head["kern"], head["crit"]
+    dom = kern[crit]
+    achieved = dom["hbm_GBps"] or 0.0
+    value = head["value"]
     out = {
         "metric": "KV migration GB/s (D2H+H2D) vs host-link peak; gather/scatter HBM GB/s",
         "value": round(value, 3),
@@ -620,30 +735,22 @@ def main() -> int:
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(elapsed / args.steps * 1e3, 3),
+        "ms_per_step": round(head["elapsed"] / args.steps * 1e3, 3),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "u8",
         "data": "synthetic",
         "config": {
-            "workload": (f"{cfg.name}: {inst.P} programs, {cfg.layers} layers x {cfg.planes} planes x "
-                         f"{cfg.row_bytes} B rows ({cfg.dtype}), {cfg.block_tokens}-token blocks, "
-                         f"{g.num_blocks} pages = {g.pool_bytes / GIB:.2f} GiB pool, GPU budget {cfg.gpu_pct}% "
-                         f"of KV bytes, CPU tier {args.cpu_gib:g} GiB in a {args.arena_gib:g} GiB pinned arena; "
-                         + (f"contexts scaled by {scale:g}, nothing placed before step 0, then per step the GPU "
-                            f"budget swings {cfg.pct_swing[0]:g}+-{cfg.pct_swing[1]:g}% and "
-                            f"{cfg.flip_frac:.0%} of programs flip phase" if churn else
-                            "steps alternate drawn / reversed idleness windows" if args.schedule == "reverse" else
-                            "each step the CPU-tier programs become the busiest (idleness given)")),
-            "copy_mode": {0: "auto", 1: "kernel", 2: "copy-engine"}[int(last_mode)],
+            "workload": head["desc"],
+            "copy_mode": {0: "auto", 1: "kernel", 2: "copy-engine"}[head["copy_mode"]],
             "hw_queues": int(os.environ["GPU_MAX_HW_QUEUES"]),
-            "gpu_budget_bytes": bg,
-            "cpu_budget_bytes": bc,
-            "bytes_per_step": int(moved / max(args.steps, 1)),
+            "gpu_budget_bytes": head["bg"],
+            "cpu_budget_bytes": head["bc"],
+            "bytes_per_step": int(head["moved"] / max(args.steps, 1)),
         },
         "hostlink": {**peaks, "frac_of_bidir_peak": round(value / peaks["bidir_GBps"], 4),
-                     "frac_of_mix_bound": round(mix_bound_s / elapsed, 4),
+                     "frac_of_mix_bound": round(head["mix_bound_s"] / head["elapsed"], 4),
                      "mix_bound": ("lower bound on the timed steps' time on this link, per step max(out / d2h, "
                                    "in / h2d, (out + in) / bidir), summed; frac_of_mix_bound = that bound over the "
                                    "measured time (equals frac_of_bidir_peak when every step moves as much each way)")},
@@ -660,27 +767,31 @@ def main() -> int:
             "note": ("whole-system serving gains of the method, context only; the paper reports no KV migration "
                      "or gather/scatter bandwidth, hence vs_baseline null"),
         },
-        "direction_ms_per_step": {"swap_out": round(span[0] / args.steps, 2), "swap_in": round(span[1] / args.steps, 2)},
-        "plan_us_in_step": round(span[2] / args.steps * 1e3, 1),
+        "direction_ms_per_step": {"swap_out": round(head["span"][0] / args.steps, 2),
+                                  "swap_in": round(head["span"][1] / args.steps, 2)},
+        "plan_us_in_step": round(head["span"][2] / args.steps * 1e3, 1),
+        "other_workloads": others or None,
         "plan": plan,
         "replica_admit": replica,
         "cpu_baseline": cpu,
-        "verify": verify,
+        "verify": head["verify"],
         "evict_order": evict,
     }
     print(json.dumps(out), flush=True)
-    tp.close()
     return 0
 
 
-def verify_sampled(inst, tp, bank, history, bg, bc, valid, np, run_content):
+def verify_state(inst, tp, bank_dev, history, bg, bc, valid, np):
     """Checks of the final state that need no reference implementation (exact
     parity with the oracle at these sizes is a GPU test): every page owned at
     most once and never also free, owned + free pages = the pool, programs off
     the GPU own no page, both budgets respected, each step's page accounting
-    consistent, and sampled runs of resident programs equal to their
-    content-addressed value (the input run of the same program, block and
-    plane: the copy rule of a swap)."""
+    consistent, and every byte of every resident run of the programs whose KV
+    is defined (all pages of GPU-resident programs, all CPU-tier host buffers)
+    equal to its content-addressed value -- the input run of the same program,
+    block and plane: the copy rule of a swap."""
+    from workload import check_tier_bytes
+
     g = inst.geom
     tbl, tier, free = tp.state()
     off = inst.tbl_off
@@ -697,24 +808,11 @@ def verify_sampled(inst, tp, bank, history, bg, bc, valid, np, run_content):
     for t, h in enumerate(history):
         if h["pages_free_before"] + h["pages_released"] - h["pages_in"] - h["pages_admit"] != h["pages_free_after"]:
             return {"ok": False, "what": "page accounting", "step": t}
-    rng = np.random.default_rng(7)
-    checked = 0
-    planes = tp.pool.view(g.nplanes, g.num_blocks, g.run_bytes)
-    for p in np.flatnonzero(valid & (tier != 2) & (inst.nblk > 0)):
-        for _ in range(8):
-            i = int(rng.integers(0, inst.nblk[p]))
-            q = int(rng.integers(0, g.nplanes))
-            expect = run_content(bank, g.run_bytes, p, i, q)[0]
-            if tier[p] == 0:
-                got = planes[q, int(tbl[off[p] + i])].cpu().numpy()
-            else:
-                hv = tp.host_view(int(p))
-                got = hv[(q * int(inst.nblk[p]) + i) * g.run_bytes:(q * int(inst.nblk[p]) + i + 1) * g.run_bytes]
-            if not np.array_equal(got, expect):
-                return {"ok": False, "what": "bytes", "program": int(p), "block": i, "plane": q}
-            checked += 1
-    return {"ok": True, "steps": len(history), "runs_checked": checked,
-            "programs_checked": int((valid & (tier != 2) & (inst.nblk > 0)).sum())}
+    r = check_tier_bytes(tp.pool, g, off, tbl, tier, bank_dev, tp.host_view, programs=valid)
+    if not r["ok"]:
+        return {"ok": False, "what": "bytes", **r}
+    return {"ok": True, "steps": len(history), "runs_checked": r["gpu_runs"] + r["host_runs"],
+            "bytes_checked": r["bytes"], "programs_checked": int((valid & (tier != 2) & (inst.nblk > 0)).sum())}
 
 
 if __name__ == "__main__":

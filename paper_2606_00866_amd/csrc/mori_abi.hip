@@ -689,8 +689,14 @@ extern "C" int mori_kv_swap_in(mori_ctx* ctx, const uint64_t* host_src, uint32_t
     SwapArgs a = swap_args(ctx, 1);
     uint32_t j = 0;
     uint64_t c = 0;
-    for (uint64_t u0 = 0; u0 < total; u0 += cu, ++c) {
-      const uint64_t u1 = std::min(total, u0 + cu);
+    // The first chunk is half a staging half: the copy engines then finish
+    // the swap-in's chunks half a chunk period away from the swap-out's, so
+    // a scatter kernel (launched when its chunk has arrived) falls between
+    // the gather kernels (launched when a chunk has left) instead of on top
+    // of them, and neither shares HBM with the other.
+    const uint64_t cu0 = total > cu ? std::max<uint64_t>(1, cu / 2) : cu;
+    for (uint64_t u0 = 0, u1 = 0; u0 < total; u0 = u1, ++c) {
+      u1 = std::min(total, u0 + (c == 0 ? cu0 : cu));
       const int h = (int)(c & 1);
       uint8_t* half = ctx->staging[1] + (uint64_t)h * cu * run;
       if (c >= 2) HIP_TRY(ctx, hipStreamWaitEvent(cs, ctx->ev_half_free[1][h], 0));

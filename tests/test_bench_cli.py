@@ -39,3 +39,39 @@ def test_link_bound_is_a_lower_bound_per_step():
     for o, i in ((1e9, 2e9), (7e9, 3e9), (5e9, 5e9)):
         t = bench.link_bound_s(o, i, pk)
         assert t >= o / 50e9 and t >= i / 60e9 and t >= (o + i) / 100e9
+
+
+def test_steady_two_way_window_counts_bytes_done():
+    sys.path.insert(0, ROOT)
+    import bench
+
+    ends = [1.0, 2.0, 3.0, 4.0]  # four chunks of 10 bytes, one per second
+    assert bench.bytes_done_by(ends, 4.0, 10) == 40.0
+    assert bench.bytes_done_by(ends, 2.0, 10) == 20.0
+    assert bench.bytes_done_by(ends, 2.5, 10) == 25.0
+    assert bench.bytes_done_by(ends, 0.5, 10) == 5.0
+    assert bench.bytes_done_by([1.0, 3.0], 2.0, 10) == 15.0  # the straddling chunk's own span
+    assert bench.bytes_done_by(ends, 9.0, 10) == 40.0
+
+
+def test_rotation_schedule_gives_each_tier_its_set():
+    import numpy as np
+
+    sys.path.insert(0, ROOT)
+    import bench
+    from oracle import oracle
+    from workload import MLA, make_instance, rotation_windows
+
+    inst = make_instance(MLA, scale=1 / 64)
+    window_of = bench.schedule_windows(np, inst, "rotate", 4)
+    rot = rotation_windows(MLA.seed, inst.P, 4)
+    tier = np.arange(inst.P, dtype=np.uint8) % 3
+    w = window_of(2, tier)
+    for p in (0, 1, 2, 7):
+        assert np.array_equal(w[p], rot[2, bench.ROT_SET_OF_TIER[tier[p]], p])
+    # CPU tier busiest, then GPU, then Waiting, by Eq. 1
+    rc, iota = oracle.idleness(w)
+    assert rc == oracle.OK
+    assert iota[tier == 1].max() < iota[tier == 0].min() and iota[tier == 0].max() < iota[tier == 2].min()
+    rev = bench.schedule_windows(np, inst, "reverse", 4)
+    assert np.array_equal(rev(1, tier), inst.window[:, :, ::-1])

@@ -589,6 +589,37 @@ def test_runs_per_pass(row_bytes, tokens, mode):
         pair.close()
 
 
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("row_bytes,tokens,staging_runs", [(1152, 64, 0), (1152, 64, 3), (768, 64, 5), (2560, 16, 2),
+                                                           (1152, 32, 0)],
+                         ids=["72KiB", "72KiB-small-staging", "48KiB", "40KiB", "36KiB"])
+def test_runs_ending_inside_a_pass(row_bytes, tokens, staging_runs, mode):
+    """Runs longer than a workgroup pass that are not whole passes (72 KiB as
+    in the compressed-latent workload, 48, 40 and 36 KiB) are copied as a flat
+    stream of slices that cross run and program boundaries: every byte lands
+    where the oracle puts it, three steps both ways, in both copy modes and
+    with staging halves of a few runs (slices then also start at chunk
+    boundaries)."""
+    rng = np.random.default_rng(row_bytes * 7 + tokens + staging_runs)
+    geom = Geometry(layers=3, planes=1, block_tokens=tokens, row_bytes=row_bytes, num_blocks=0)
+    inst = random_instance(rng, P=30, max_blocks=9, geom=geom, tier_p=(0.5, 0.3, 0.2), extra_free=12)
+    log(f"runs inside a pass: run={row_bytes * tokens} B mode={mode} staging runs={staging_runs}")
+    pair = Pair(inst, seed=row_bytes + tokens, staging_bytes=2 * staging_runs * inst.geom.run_bytes)
+    try:
+        bb = inst.geom.block_bytes
+        # drawn, reversed, then another program's windows for each program
+        wins = [inst.window, inst.window[:, :, ::-1].copy(), np.ascontiguousarray(inst.window[rng.permutation(inst.P)])]
+        moved = 0
+        for w in wins:
+            res, plan = pair.step(gpu_bytes=inst.geom.num_blocks * bb * 2 // 3 // bb * bb,
+                                  cpu_bytes=inst.total_bytes // 3 // bb * bb, window=w, mode=mode)
+            assert res.rc == oracle.OK and plan is not None
+            moved += (plan.n_in > 0) + (plan.n_out > 0)
+        assert moved >= 4  # swaps in both directions in at least two of the steps
+    finally:
+        pair.close()
+
+
 SUMMARY = ("m_gpu", "m_cpu", "n_out", "n_in", "n_drop_gpu", "n_drop_cpu", "n_admit_gpu", "n_admit_cpu", "pages_out",
            "pages_in", "pages_admit", "pages_free_before", "pages_released", "pages_recycled", "pages_free_after",
            "bytes_out", "bytes_in", "gpu_bytes_after", "cpu_bytes_after")
