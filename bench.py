@@ -78,6 +78,10 @@ def parse():
     ap.add_argument("--no-plan", action="store_true", help="skip the rank/partition latency leg")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--hw-queues", type=int, default=8, help="GPU_MAX_HW_QUEUES for this process (read at start)")
+    ap.add_argument("--serial-swaps", action="store_true",
+                    help="for kernel traces: the swap-in on the swap-out's stream, so (with --hw-queues 4) every "
+                         "kernel and copy runs in order and no kernel shares the GPU with another (not a "
+                         "throughput configuration)")
     return ap.parse_args()
 
 
@@ -699,7 +703,8 @@ def main() -> int:
     peaks = measure_peaks(torch, M, s_out, s_in)
     log(f"peaks {peaks}")
 
-    head = run_workload(args, cfg.name, schedule, args.steps, args.warmup, s_out, s_in, peaks, torch, np, M)
+    head = run_workload(args, cfg.name, schedule, args.steps, args.warmup, s_out, s_out if args.serial_swaps else s_in,
+                        peaks, torch, np, M)
     others = {}
     for name in [w for w in args.extra.split(",") if w and w != cfg.name]:
         o = run_workload(args, name, "rotate" if name == "mla" else "reverse", args.extra_steps, args.warmup, s_out,
