@@ -95,6 +95,7 @@ struct SwapArgs {
   uint8_t* staging;         // non-null: chunk staging buffer (copy-engine mode)
   uint64_t u_begin, u_end;  // staging mode: unit range of the chunk
   uint32_t part;            // swap-in: 0 all slots, 1 slots < free-before, 2 slots >= free-before
+  uint32_t host_link;       // 1: the other side is pinned host memory (kernel-direct mode over the host link)
 };
 
 struct TranslateArgs {

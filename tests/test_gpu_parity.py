@@ -567,12 +567,18 @@ def test_pools_around_the_tile_scan_switch(target):
 
 
 @pytest.mark.parametrize("mode", MODES)
-@pytest.mark.parametrize("row_bytes,tokens", [(2048, 16), (1024, 16), (256, 16), (128, 16), (16, 4)],
-                         ids=["32KiB", "16KiB", "4KiB", "2KiB", "64B"])
+@pytest.mark.parametrize("row_bytes,tokens", [(2048, 16), (1536, 16), (1024, 16), (512, 16), (256, 16), (128, 16),
+                                               (16, 4)],
+                         ids=["32KiB", "24KiB", "16KiB", "8KiB", "4KiB", "2KiB", "64B"])
 def test_runs_per_pass(row_bytes, tokens, mode):
-    """Runs of 32 KiB (one per workgroup pass), 16, 4 and 2 KiB (two, four and
-    eight per pass) and 64 B (sixteen): every byte lands where the oracle puts
-    it, three steps with swaps both ways."""
+    """Runs of 32 KiB (between HBM buffers one round of four vectors per
+    thread, half of them past the run's end), 24 KiB and 16 KiB (one vector
+    per thread per round: two rounds, the second half past the end, and one;
+    over the host link two runs per workgroup), and runs a workgroup copies
+    several at a time, one vector per thread: 8, 4 and 2 KiB (two, four and
+    eight per pass) and 64 B (sixteen, most threads past the end): every byte
+    lands where the oracle puts it, three steps with swaps both ways, in both
+    copy modes."""
     rng = np.random.default_rng(row_bytes * 100 + tokens)
     geom = Geometry(layers=2, planes=2, block_tokens=tokens, row_bytes=row_bytes, num_blocks=0)
     inst = random_instance(rng, P=40, max_blocks=12, geom=geom, tier_p=(0.5, 0.3, 0.2), extra_free=20)
@@ -591,15 +597,19 @@ def test_runs_per_pass(row_bytes, tokens, mode):
 
 @pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("row_bytes,tokens,staging_runs", [(1152, 64, 0), (1152, 64, 3), (768, 64, 5), (2560, 16, 2),
-                                                           (1152, 32, 0)],
-                         ids=["72KiB", "72KiB-small-staging", "48KiB", "40KiB", "36KiB"])
+                                                           (1152, 32, 0), (1024, 64, 0), (1536, 64, 2), (1792, 64, 0),
+                                                           (2048, 64, 3), (2176, 64, 0), (4096, 64, 2)],
+                         ids=["72KiB", "72KiB-small-staging", "48KiB", "40KiB", "36KiB", "64KiB", "96KiB", "112KiB",
+                              "128KiB", "136KiB", "256KiB"])
 def test_runs_ending_inside_a_pass(row_bytes, tokens, staging_runs, mode):
-    """Runs longer than a workgroup pass that are not whole passes (72 KiB as
-    in the compressed-latent workload, 48, 40 and 36 KiB) are copied as a flat
-    stream of slices that cross run and program boundaries: every byte lands
-    where the oracle puts it, three steps both ways, in both copy modes and
-    with staging halves of a few runs (slices then also start at chunk
-    boundaries)."""
+    """Long runs, which between HBM buffers a workgroup copies one at a time
+    in rounds of four vectors per thread (64 KiB): 36, 40 and 48 KiB (one
+    round, the rest of it past the run's end), 64 KiB (exactly one), 72 KiB as
+    in the compressed-latent workload (a full round and one of 8 KiB), 96 and
+    112 KiB, 128 KiB (exactly two), 136 KiB (three, the last mostly past the
+    end) and 256 KiB (four); over the host link two at a time in rounds of
+    8 KiB: every byte lands where the oracle puts it, three steps both ways, in
+    both copy modes and with staging halves of a few runs."""
     rng = np.random.default_rng(row_bytes * 7 + tokens + staging_runs)
     geom = Geometry(layers=3, planes=1, block_tokens=tokens, row_bytes=row_bytes, num_blocks=0)
     inst = random_instance(rng, P=30, max_blocks=9, geom=geom, tier_p=(0.5, 0.3, 0.2), extra_free=12)
