@@ -353,6 +353,22 @@ def link_bound_s(out_bytes: int, in_bytes: int, peaks: dict) -> float:
                (out_bytes + in_bytes) / (peaks["bidir_GBps"] * 1e9))
 
 
+def split_model_s(out_bytes: int, in_bytes: int, peaks: dict) -> float:
+    """Time of one step's copies if both directions start together and run
+    flat out: at the two-way split measured in the same run (bidir_split)
+    until the smaller direction is done, then the larger one alone at its
+    one-direction rate.  A model of two unpaced copy streams, not a bound
+    (pacing the smaller direction could beat it when the two differ)."""
+    rd, rh = peaks["bidir_split_GBps"]["d2h"] * 1e9, peaks["bidir_split_GBps"]["h2d"] * 1e9
+    alone_d, alone_h = peaks["d2h_GBps"] * 1e9, peaks["h2d_GBps"] * 1e9
+    if out_bytes == 0 or in_bytes == 0:
+        return out_bytes / alone_d + in_bytes / alone_h
+    t_d, t_h = out_bytes / rd, in_bytes / rh
+    if t_d <= t_h:
+        return t_d + (in_bytes - rh * t_d) / alone_h
+    return t_h + (out_bytes - rd * t_h) / alone_d
+
+
 def evict_inputs(np, N):
     """Synthetic block metadata of the eviction-order leg (Sec. 4.3.2): N
     blocks of 1024 programs, half the timestamps tied, variable block sizes,
@@ -627,6 +643,7 @@ def run_workload(args, name, schedule, steps, warmup, s_out, s_in, peaks, torch,
     M.mori_profile(tp.ctx, False)
     value = moved / elapsed / 1e9
     mix_bound_s = sum(link_bound_s(h["bytes_out"], h["bytes_in"], peaks) for h in history[-steps:])
+    split_s = sum(split_model_s(h["bytes_out"], h["bytes_in"], peaks) for h in history[-steps:])
     log(f"timed {steps} steps: {moved / GIB:.2f} GiB in {elapsed:.3f} s -> {value:.2f} GB/s")
 
     # dominant kernel: the gather/scatter kernel of the direction on the step's
@@ -656,7 +673,7 @@ def run_workload(args, name, schedule, steps, warmup, s_out, s_in, peaks, torch,
                "Waiting idle; redrawn per step), Eq. 1 computed on the device"))
     out = {"name": cfg.name, "value": value, "elapsed": elapsed, "moved": moved, "kern": kern, "crit": crit,
            "span": span, "verify": verify, "desc": desc, "copy_mode": int(last_mode), "bg": bg, "bc": bc,
-           "mix_bound_s": mix_bound_s, "inst": inst}
+           "mix_bound_s": mix_bound_s, "split_s": split_s, "inst": inst}
     tp.close()
     del tp, pool, bank_dev, wins
     torch.cuda.synchronize()
@@ -758,7 +775,12 @@ def main() -> int:
                      "frac_of_mix_bound": round(head["mix_bound_s"] / head["elapsed"], 4),
                      "mix_bound": ("lower bound on the timed steps' time on this link, per step max(out / d2h, "
                                    "in / h2d, (out + in) / bidir), summed; frac_of_mix_bound = that bound over the "
-                                   "measured time (equals frac_of_bidir_peak when every step moves as much each way)")},
+                                   "measured time (equals frac_of_bidir_peak when every step moves as much each way)"),
+                     "split_model_over_measured": round(head["split_s"] / head["elapsed"], 4),
+                     "split_model": ("per step, both directions started together at the measured two-way split "
+                                     "(bidir_split) until the smaller is done, then the larger alone at its "
+                                     "one-direction rate, summed; over the measured time (a model of two unpaced "
+                                     "copy streams, not a bound: above 1 the steps beat it)")},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": stored_traffic(cfg.name, crit),
                      "algorithmic_bytes_per_launch": int(2 * dom["payload_bytes"] / max(dom["launches"], 1)),

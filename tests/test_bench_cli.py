@@ -41,6 +41,26 @@ def test_link_bound_is_a_lower_bound_per_step():
         assert t >= o / 50e9 and t >= i / 60e9 and t >= (o + i) / 100e9
 
 
+def test_split_model_of_two_unpaced_copy_streams():
+    """Both directions at the measured two-way split until the smaller is
+    done, then the larger alone: worked by hand."""
+    sys.path.insert(0, ROOT)
+    import bench
+
+    pk = {"d2h_GBps": 60.0, "h2d_GBps": 60.0, "bidir_split_GBps": {"d2h": 40.0, "h2d": 50.0}}
+    assert bench.split_model_s(0, 0, pk) == 0.0
+    assert bench.split_model_s(12e9, 0, pk) == 12e9 / 60e9              # one direction: its own rate
+    assert bench.split_model_s(0, 6e9, pk) == 6e9 / 60e9
+    # D2H 8 GB, H2D 5 GB: H2D done at 0.1 s (D2H has moved 4 GB), 4 GB left at 60 GB/s
+    assert abs(bench.split_model_s(8e9, 5e9, pk) - (0.1 + 4e9 / 60e9)) < 1e-12
+    # D2H 2 GB, H2D 10 GB: D2H done at 0.05 s (H2D has moved 2.5 GB), 7.5 GB left at 60 GB/s
+    assert abs(bench.split_model_s(2e9, 10e9, pk) - (0.05 + 7.5e9 / 60e9)) < 1e-12
+    # never below the link bound built from the same figures
+    pk2 = dict(pk, bidir_GBps=90.0)
+    for o, i in ((1e9, 2e9), (7e9, 3e9), (5e9, 5e9)):
+        assert bench.split_model_s(o, i, pk) >= bench.link_bound_s(o, i, pk2) - 1e-12
+
+
 def test_steady_two_way_window_counts_bytes_done():
     sys.path.insert(0, ROOT)
     import bench
