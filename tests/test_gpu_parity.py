@@ -320,20 +320,25 @@ def test_profile_counters(mode):
         pair.close()
 
 
-@pytest.mark.parametrize("where,mode", [("device", M.MORI_COPY_AUTO), ("two_ranges", M.MORI_COPY_KERNEL),
-                                        ("two_ranges", M.MORI_COPY_CE)])
-def test_buffers_in_other_registered_ranges(where, mode):
+@pytest.mark.parametrize("where,mode,row_bytes,tokens",
+                         [("device", M.MORI_COPY_AUTO, 64, 4), ("device", M.MORI_COPY_AUTO, 1152, 64),
+                          ("device", M.MORI_COPY_AUTO, 1024, 16), ("two_ranges", M.MORI_COPY_KERNEL, 64, 4),
+                          ("two_ranges", M.MORI_COPY_CE, 64, 4)],
+                         ids=["device-256B", "device-72KiB", "device-16KiB", "two_ranges-kernel", "two_ranges-ce"])
+def test_buffers_in_other_registered_ranges(where, mode, row_bytes, tokens):
     """CPU-tier buffers in a registered device-memory range (AUTO then resolves
-    to the kernels at the device grid) or alternating between two pinned host
-    ranges registered beside the pool's arena: tables, tiers, free map, resident
-    pages and every buffer byte equal the oracle's over three steps; then the
-    range limit (ENOSPC) and unknown memory (EINVAL)."""
+    to the kernels at the device grid and its copy shapes: 256 B runs sixteen
+    to a workgroup, 72 KiB runs in rounds of four vectors per thread, 16 KiB
+    runs one vector per thread) or alternating between two pinned host ranges
+    registered beside the pool's arena: tables, tiers, free map, resident pages
+    and every buffer byte equal the oracle's over three steps; then the range
+    limit (ENOSPC) and unknown memory (EINVAL)."""
     import ctypes
 
     from workload import fill_pool_np, make_bank, program_host_content
 
     rng = np.random.default_rng(77)
-    geom = Geometry(layers=2, planes=2, block_tokens=4, row_bytes=64, num_blocks=0)
+    geom = Geometry(layers=2, planes=2, block_tokens=tokens, row_bytes=row_bytes, num_blocks=0)
     inst = random_instance(rng, P=24, max_blocks=10, geom=geom, tier_p=(0.55, 0.45), extra_free=8)
     g, bb = inst.geom, inst.geom.block_bytes
     bank = make_bank(3, inst.dtype, g.run_bytes)
