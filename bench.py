@@ -589,19 +589,26 @@ def run_workload(args, name, schedule, steps, warmup, s_out, s_in, peaks, torch,
 
     span = [0.0, 0.0, 0.0]  # summed device time from the step's start to the end of swap-out / swap-in / plan
 
-    def one_step(t, timed=False):
+    last_w = [None]  # the window tensor of the last step
+
+    def one_step(t, timed=False, budget=None, window=None):
         e0, e_plan, e_out, e_in = (torch.cuda.Event(enable_timing=True) for _ in range(4))
         e0.record(s_out)
-        if churn:
+        if window is not None:  # an explicit step (the one-way pair after the timed steps)
+            check(tp.rank_partition(gpu_bytes=budget, cpu_bytes=bc, window=window, stream=s_out), "rank")
+        elif churn:
             bg_t, w_t = (bg, wins[0]) if t == 0 else churn_inputs[t - 1]
             step_bg[0] = bg_t
             check(tp.rank_partition(gpu_bytes=bg_t, cpu_bytes=bc, window=w_t, stream=s_out), "rank")
+            last_w[0] = w_t
         elif schedule == "rotate":  # each program's window from its tier's set: Eq. 1 on the device
             with torch.cuda.stream(s_out):
                 w_t = rot[t][rot_sel[tp.tier.long()], prog_ids]
             check(tp.rank_partition(gpu_bytes=bg, cpu_bytes=bc, window=w_t, stream=s_out), "rank")
+            last_w[0] = w_t
         else:
             check(tp.rank_partition(gpu_bytes=bg, cpu_bytes=bc, window=wins[t % 2], stream=s_out), "rank")
+            last_w[0] = wins[t % 2]
         e_plan.record(s_out)
         rc, p = tp.plan_wait()
         if rc != M.MORI_OK:
@@ -646,6 +653,28 @@ def run_workload(args, name, schedule, steps, warmup, s_out, s_in, peaks, torch,
     split_s = sum(split_model_s(h["bytes_out"], h["bytes_in"], peaks) for h in history[-steps:])
     log(f"timed {steps} steps: {moved / GIB:.2f} GiB in {elapsed:.3f} s -> {value:.2f} GB/s")
 
+    # One way at a time, after the timed steps: every CPU-tier program back to
+    # the GPU (a GPU budget of all KV bytes: H2D only), then the last timed
+    # step's budgets and windows again, which put the same programs on the CPU
+    # tier (D2H only) and so restore its tiers; each over its wall time (plan
+    # included), against the same direction's measured peak.
+    one_way = None
+    if not churn and inst.total_bytes <= g.num_blocks * g.block_bytes:
+        one_way = []
+        w_keep = last_w[0]
+        for label, budget in (("H2D", inst.total_bytes), ("D2H", bg)):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            p = one_step(warmup + steps, budget=budget, window=w_keep)
+            dt = time.perf_counter() - t0
+            nb, other = (p.bytes_in, p.bytes_out) if label == "H2D" else (p.bytes_out, p.bytes_in)
+            rate = nb / dt / 1e9
+            peak = peaks["h2d_GBps"] if label == "H2D" else peaks["d2h_GBps"]
+            one_way.append({"direction": label, "bytes": int(nb), "other_direction_bytes": int(other),
+                            "ms": round(dt * 1e3, 2), "GBps": round(rate, 2),
+                            "frac_of_one_way_peak": round(rate / peak, 4)})
+        log(f"one way: {one_way}")
+
     # dominant kernel: the gather/scatter kernel of the direction on the step's
     # critical path (the direction whose work ends last)
     kern = []
@@ -673,7 +702,7 @@ def run_workload(args, name, schedule, steps, warmup, s_out, s_in, peaks, torch,
                "Waiting idle; redrawn per step), Eq. 1 computed on the device"))
     out = {"name": cfg.name, "value": value, "elapsed": elapsed, "moved": moved, "kern": kern, "crit": crit,
            "span": span, "verify": verify, "desc": desc, "copy_mode": int(last_mode), "bg": bg, "bc": bc,
-           "mix_bound_s": mix_bound_s, "split_s": split_s, "inst": inst}
+           "mix_bound_s": mix_bound_s, "split_s": split_s, "one_way": one_way, "inst": inst}
     tp.close()
     del tp, pool, bank_dev, wins
     torch.cuda.synchronize()
@@ -776,6 +805,7 @@ def main() -> int:
                      "mix_bound": ("lower bound on the timed steps' time on this link, per step max(out / d2h, "
                                    "in / h2d, (out + in) / bidir), summed; frac_of_mix_bound = that bound over the "
                                    "measured time (equals frac_of_bidir_peak when every step moves as much each way)"),
+                     "one_way_step": head["one_way"],
                      "split_model_over_measured": round(head["split_s"] / head["elapsed"], 4),
                      "split_model": ("per step, both directions started together at the measured two-way split "
                                      "(bidir_split) until the smaller is done, then the larger alone at its "
