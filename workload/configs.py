@@ -68,6 +68,13 @@ LLAMA3_70B = KVConfig("llama3_70b", layers=80, planes=2, block_tokens=16, row_by
 LLAMA3_70B_TP2 = KVConfig("llama3_70b_tp2", layers=80, planes=2, block_tokens=16, row_bytes=4 * 128 * 2,
                           dtype="bf16", programs=64, ctx_kind="lognormal", ctx_median=6144, ctx_lo=2048,
                           ctx_hi=24576, busy_frac=0.3, gpu_pct=60.0, frag="chunked", seed=3)
+# the same share at tensor parallelism 4 and 8: 2 and 1 KV heads per rank, 512-B and 256-B rows, 8 and 4 KiB runs
+LLAMA3_70B_TP4 = KVConfig("llama3_70b_tp4", layers=80, planes=2, block_tokens=16, row_bytes=2 * 128 * 2,
+                          dtype="bf16", programs=64, ctx_kind="lognormal", ctx_median=6144, ctx_lo=2048,
+                          ctx_hi=24576, busy_frac=0.3, gpu_pct=60.0, frag="chunked", seed=3)
+LLAMA3_70B_TP8 = KVConfig("llama3_70b_tp8", layers=80, planes=2, block_tokens=16, row_bytes=1 * 128 * 2,
+                          dtype="bf16", programs=64, ctx_kind="lognormal", ctx_median=6144, ctx_lo=2048,
+                          ctx_hi=24576, busy_frac=0.3, gpu_pct=60.0, frag="chunked", seed=3)
 MLA = KVConfig("mla", layers=61, planes=1, block_tokens=64, row_bytes=576 * 2, dtype="bf16",
                programs=256, ctx_kind="lognormal", ctx_median=8192, ctx_lo=1024, ctx_hi=32768,
                busy_frac=0.5, gpu_pct=40.0, frag="chunked", seed=4)
@@ -76,4 +83,5 @@ CHURN = KVConfig("churn", layers=32, planes=2, block_tokens=16, row_bytes=8 * 12
                  busy_frac=0.5, gpu_pct=55.0, frag="shuffled", seed=5, steps=100, flip_frac=0.1,
                  pct_swing=(55.0, 10.0))
 
-CONFIGS = {c.name: c for c in (TINY, LLAMA3_8B, LLAMA3_70B, LLAMA3_70B_TP2, MLA, CHURN)}
+CONFIGS = {c.name: c for c in (TINY, LLAMA3_8B, LLAMA3_70B, LLAMA3_70B_TP2, LLAMA3_70B_TP4, LLAMA3_70B_TP8, MLA,
+                                CHURN)}
