@@ -152,6 +152,35 @@ def test_full_size_workload(cfg):
         h.close()
 
 
+@pytest.mark.parametrize("cfg", [MLA, LLAMA3_70B_TP2], ids=lambda c: c.name)
+def test_full_size_kernel_direct(cfg):
+    """Kernel-direct swaps at full size: the gather stores into, and the
+    scatter loads from, the pinned CPU tier over the host link (two runs per
+    workgroup, one vector per thread per round; the swap-in in two launches
+    around the swap-out's event).  Drawn windows, then twice given idleness
+    that ranks the CPU tier busiest (both directions move); every byte
+    compared after each step."""
+    inst = make_instance(cfg)
+    bg = budget_bytes(inst.total_bytes, cfg.gpu_pct)
+    bc = 28 * GIB
+    log(f"{cfg.name} kernel-direct: P={inst.P} pool {inst.geom.pool_bytes / GIB:.1f} GiB")
+    h = Harness(inst, arena_bytes=60 * GIB)
+    try:
+        moved_both = 0
+        for t in range(3):
+            if t == 0:
+                plan = h.step(inst.window, bg, bc, mode=M.MORI_COPY_KERNEL)
+            else:  # CPU-tier programs busiest, then GPU-tier ones, Waiting last
+                iota = np.array([0.5, 0.1, 0.9], np.float32)[h.tier]
+                plan = h.step(None, bg, bc, mode=M.MORI_COPY_KERNEL, iota=iota)
+            moved_both += plan.n_in > 0 and plan.n_out > 0
+            log(f"  step {t}: out {plan.bytes_out / GIB:.2f} GiB in {plan.bytes_in / GIB:.2f} GiB")
+        assert moved_both == 2
+        assert M.mori_query(h.tp.ctx, M.MORI_Q_LAST_MODE) == (M.MORI_OK, M.MORI_COPY_KERNEL)
+    finally:
+        h.close()
+
+
 def test_churn_scaled():
     """Churn at 8% of its context lengths (about 46 GiB of KV, a 30 GiB pool and
     a CPU tier of a quarter of the KV bytes): 100 steps, both directions each step."""
